@@ -1,0 +1,207 @@
+/*
+ * bkmoo — bucket-level gradient-conflict resolution on MI355X (gfx950).
+ *
+ * The operation (Section 3.2 and Algorithm 1 of "Multilingual Fine-Tuning
+ * via Localized Gradient Conflict Resolution"): the flattened parameter
+ * vector is cut into B contiguous buckets; every language (task) i of K has
+ * its own gradient x_i over all N parameters.  For each bucket b the local
+ * gradient set is the K slices x_i[o_b : o_{b+1}], a small multi-objective
+ * problem is solved on that set alone, and the bucket's update is a weighted
+ * sum of the slices,
+ *
+ *     d[o_b : o_{b+1}] = sum_i w_{b,i} x_i[o_b : o_{b+1}],
+ *
+ * with the updates of all buckets concatenated into d (Algorithm 1, final
+ * step).  Every bucket-level method only sees its gradients through their
+ * inner products, so the work splits into
+ *
+ *     gram    G_b[i][j] = <x_i, x_j> over the bucket      (streams K*N)
+ *     solve   G_b -> w_b (MGDA, PCGrad, CAGrad, or mean)  (K x K work)
+ *     combine d = sum_i w_{b,i} x_i                        (streams K*N, writes N)
+ *
+ * and resolve runs the three in order on one stream.
+ *
+ * Notation: the paper writes T for the number of languages and K for the
+ * number of buckets; this interface writes K for the languages and B for the
+ * buckets.
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are DEVICE pointers unless marked (host).  The caller owns and
+ *     allocates every buffer; the library never allocates, frees or
+ *     synchronises inside these calls, and all work is queued on `stream`
+ *     (asynchronous; results are valid once the stream reaches that point).
+ *   - grads is a HOST array of K device pointers, one per task, each to N
+ *     elements of dtype `dt`.  A contiguous [K][N] buffer is passed as
+ *     base + i*N*elem_size.  Rows need natural alignment (4 bytes for f32,
+ *     2 for bf16); 16-byte alignment of every row at the same phase enables
+ *     128-bit loads, otherwise a scalar path is used.
+ *   - bucket_offsets is int64[B+1] in device memory with o_0 = 0, o_B = N and
+ *     o_b <= o_{b+1} (empty buckets are allowed).  Offsets are checked on the
+ *     device; invalid offsets set BKMOO_DEVERR_OFFSETS in the workspace error
+ *     word (see bkmoo_read_device_error), make every Gram entry NaN and leave
+ *     `out` untouched.  No memory outside [0, N) is ever touched.
+ *   - Inputs are converted exactly to fp32; inner products accumulate in fp32
+ *     per lane and in fp64 across lanes, waves and chunks, in a fixed order:
+ *     results are bitwise reproducible for identical inputs on the same
+ *     device model, independent of the launch grid.
+ *   - Non-finite inputs propagate (a NaN in a bucket makes its Gram, weights
+ *     and update NaN); nothing is filtered.
+ *   - Synchronous argument errors are returned before anything is queued.
+ *     HIP launch failures return BKMOO_EHIP.
+ *   - Calls are re-entrant; concurrent calls must not share a workspace.
+ */
+#ifndef BKMOO_H
+#define BKMOO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BKMOO_OK = 0,
+  BKMOO_EINVAL = -1,        /* bad argument: null pointer, size, enum or hyper-parameter */
+  BKMOO_EUNSUPPORTED = -2,  /* well-formed but unsupported (e.g. K outside [2, 16]) */
+  BKMOO_EWORKSPACE = -3,    /* ws_bytes smaller than bkmoo_workspace_size() */
+  BKMOO_EHIP = -4           /* a HIP call or kernel launch failed */
+} bkmoo_status;
+
+typedef enum { BKMOO_F32 = 0, BKMOO_BF16 = 1 } bkmoo_dtype;
+
+/* Bucket-level strategy M of Algorithm 1, plus the plain average. */
+typedef enum {
+  BKMOO_MGDA = 0,    /* min-norm point of the bucket's gradient hull, Eq. (shard-mgda) */
+  BKMOO_PCGRAD = 1,  /* projection of conflicting pairs, Eq. (pcgrad_proj), Algorithm 1 */
+  BKMOO_CAGRAD = 2,  /* conflict-averse direction in a ball around the mean, Eq. (cagrad) */
+  BKMOO_MEAN = 3     /* averaged gradient (1/K) sum_i x_i, Section 2.1 */
+} bkmoo_method;
+
+/* Device error word bits (bkmoo_read_device_error). */
+#define BKMOO_DEVERR_OFFSETS 0x1u
+
+/* Hyper-parameters of the solve step (host struct). */
+typedef struct {
+  /* Frank-Wolfe iterations for MGDA and CAGrad (fixed count, no early
+   * exit), >= 0.  The usual value is 20. */
+  int32_t max_iter;
+  /* CAGrad conflict-aversion c in [0, 1): the update stays within
+   * c * ||mean gradient|| of the mean gradient (Eq. cagrad); Appendix E
+   * uses 0.5. */
+  double cagrad_c;
+  /* PCGrad visiting order, device int8 [B][K][K-1]: row (b, t) lists the
+   * other tasks j != t in the order task t is projected against them (the
+   * "random order" of Algorithm 1, drawn by the caller).  NULL visits them
+   * in ascending order.  A row that is not a permutation of {j != t} makes
+   * that bucket's weights NaN. */
+  const int8_t *pcgrad_order;
+} bkmoo_hparams;
+
+/*
+ * bkmoo_workspace_size — bytes of device workspace that bkmoo_gram,
+ * bkmoo_combine and bkmoo_resolve need for (K, N, B, dt).  The size is an
+ * upper bound that depends on these four values only (about 8 bytes per
+ * bucket plus 8*K*(K+1)/2 bytes per chunk of a few thousand elements).
+ * Workspace contents need no initialisation and are scratch between calls,
+ * except the error word, which the next call clears.
+ * Returns BKMOO_EINVAL for K < 2, N < 0, B < 1, bad dt or a null `bytes`
+ * (host), BKMOO_EUNSUPPORTED for K > 16.
+ */
+bkmoo_status bkmoo_workspace_size(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt, size_t *bytes);
+
+/*
+ * bkmoo_gram — per-bucket Gram matrices (the inner products every
+ * bucket-level method is defined through: ||sum_t a_t g_t||^2 = a^T G a in
+ * Eq. (shard-mgda); <g_i, g_j> in PCGrad's conflict test, Section 3.2).
+ *
+ *   gram (out) fp64 [B][K][K], row-major, symmetric:
+ *        gram[b][i][j] = sum_{n in [o_b, o_{b+1})} x_i[n] * x_j[n].
+ * Each input row is read once with 128-bit loads.
+ */
+bkmoo_status bkmoo_gram(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
+                        const int64_t *bucket_offsets, double *gram, void *workspace,
+                        size_t ws_bytes, hipStream_t stream);
+
+/*
+ * bkmoo_solve — the small per-bucket MOO problem, one wavefront per bucket,
+ * in fp64, from the Gram matrices alone.
+ *
+ *   gram    (in)  fp64 [B][K][K] (as written by bkmoo_gram)
+ *   weights (out) fp32 [B][K]: the combine coefficients, d_b = sum_i w_{b,i} g_{b,i}
+ *   aux     (out, may be NULL) fp64 [B][K]: the method's own variable
+ *
+ *   MGDA   (Eq. shard-mgda over the simplex): Frank-Wolfe started on the best
+ *          pair of tasks, argmin vertex with lowest-index ties, exact line
+ *          search, hp->max_iter iterations.  weights = aux = alpha.  For K=2
+ *          the start is already the exact minimiser.
+ *   PCGrad (Algorithm 1): d_t = g_t, projected off each g_j (visiting
+ *          order from hp->pcgrad_order) whenever <d_t, g_j> < 0; d = sum_t d_t,
+ *          tracked exactly as coefficients on the original g_i.
+ *          weights = aux = those coefficients (a sum, not a mean).
+ *   CAGrad (Eq. cagrad per bucket): the dual min over the simplex of
+ *          <g_w, g_avg> + c||g_avg|| ||g_w||, Frank-Wolfe from the uniform
+ *          point with exact line search, hp->max_iter iterations; then
+ *          d = g_avg + c||g_avg|| g_w/||g_w||, i.e. weights = 1/K + r w/||g_w||
+ *          (1/K when r = 0 or g_w vanishes); aux = w.
+ *   MEAN   weights = aux = 1/K.
+ * `hp` (host) may be NULL for MEAN; PCGrad ignores max_iter and c.
+ */
+bkmoo_status bkmoo_solve(int32_t K, int32_t B, const double *gram, bkmoo_method method,
+                         const bkmoo_hparams *hp, float *weights, double *aux, hipStream_t stream);
+
+/*
+ * bkmoo_combine — the resolved update of every bucket, concatenated
+ * (Algorithm 1: d_(k) per strategy, then d = [d_(1), ..., d_(K)]).
+ *
+ *   weights (in)  fp32 [B][K]
+ *   out     (out) N elements of out_dt, out[n] = sum_i w_{b,i} x_i[n] for n in
+ *           bucket b, summed in task order: an fp32 FMA chain for an fp32
+ *           output; for a bf16 output an fp64 chain (exact products) rounded
+ *           once to nearest-even bf16 (via round-to-odd fp32).
+ * `out` may be exactly one of the grads rows (in-place update); any other
+ * overlap with the inputs is undefined.
+ */
+bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
+                           const int64_t *bucket_offsets, const float *weights, void *out,
+                           bkmoo_dtype out_dt, void *workspace, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * bkmoo_resolve — gram, solve and combine in order on `stream` (one pass of
+ * Algorithm 1's per-bucket loop over all buckets), with no host
+ * synchronisation.  Results equal those of the three calls made one after
+ * the other.  gram, weights and aux may be NULL, in which case the
+ * intermediate values live in the workspace only.
+ */
+bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
+                           const int64_t *bucket_offsets, bkmoo_method method,
+                           const bkmoo_hparams *hp, void *out, bkmoo_dtype out_dt, double *gram,
+                           float *weights, double *aux, void *workspace, size_t ws_bytes,
+                           hipStream_t stream);
+
+/*
+ * bkmoo_read_device_error — copy the workspace's device error word into
+ * *err (host) after waiting for `stream`.  This call synchronises; it is a
+ * diagnostic, not part of the hot path.  0 means the last call that used
+ * this workspace found no error.
+ */
+bkmoo_status bkmoo_read_device_error(const void *workspace, uint32_t *err, hipStream_t stream);
+
+/*
+ * bkmoo_set_grid_override — number of workgroups the streaming kernels
+ * launch (0 restores the automatic choice: enough to fill every CU).
+ * Results do not depend on it; it exists for tuning and for tests of that
+ * independence.  Process-wide setting.
+ */
+bkmoo_status bkmoo_set_grid_override(int32_t workgroups);
+
+/* Human-readable name of a status code (static string). */
+const char *bkmoo_status_string(bkmoo_status st);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BKMOO_H */

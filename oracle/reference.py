@@ -366,6 +366,9 @@ def solve(grams: np.ndarray, method: str, max_iter: int = 20, cagrad_c: float = 
     MGDA branch), "pcgrad" (weights = column sums of C, aux = weights),
     "cagrad" (weights = 1/K + r w / ||g_w||, aux = dual w), "mean" (the
     averaged gradient of Section 2.1, weights = aux = 1/K).
+    The paper says nothing about non-finite gradients; the reading here is
+    that a bucket whose Gram matrix holds a NaN or infinity gets NaN weights
+    (and so a NaN update) rather than a silently filtered one.
     Returns (weights [B, K], aux [B, K]) float64.
     """
     grams = np.asarray(grams, dtype=np.float64)
@@ -374,6 +377,10 @@ def solve(grams: np.ndarray, method: str, max_iter: int = 20, cagrad_c: float = 
     A = np.empty((nb, k))
     for i in range(nb):
         G = grams[i]
+        if not np.all(np.isfinite(G)):
+            W[i] = np.nan
+            A[i] = np.nan
+            continue
         if method == "mgda":
             a = mgda_exact(G) if exact else mgda_fw(G, max_iter)
             W[i] = a

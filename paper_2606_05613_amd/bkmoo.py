@@ -1,0 +1,242 @@
+"""Python binding of libbkmoo (argument marshalling only).
+
+Every step of the path runs in the HIP library; this module turns torch
+tensors into the C ABI's pointers and sizes, allocates outputs and the
+workspace with torch's caching allocator when the caller passes none, and
+raises on any non-OK status.  There is no fallback: if the library is not
+built, importing this module fails.
+
+Names mirror include/bkmoo.h: workspace_size, gram, solve, combine, resolve,
+read_device_error, set_grid_override, status_string.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence, Union
+
+import torch  # must be imported before the library so both share one HIP runtime
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbkmoo.so")
+
+F32, BF16 = 0, 1
+METHODS = {"mgda": 0, "pcgrad": 1, "cagrad": 2, "mean": 3}
+DEVERR_OFFSETS = 0x1
+
+
+class BkmooError(RuntimeError):
+    pass
+
+
+class _Hparams(ctypes.Structure):
+    _fields_ = [("max_iter", ctypes.c_int32), ("cagrad_c", ctypes.c_double),
+                ("pcgrad_order", ctypes.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_05613_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    i32, i64, sz, vp, u32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_uint32
+    vpp = ctypes.POINTER(ctypes.c_void_p)
+    sig = {
+        "bkmoo_workspace_size": [i32, i64, i32, ctypes.c_int, ctypes.POINTER(sz)],
+        "bkmoo_gram": [i32, vpp, ctypes.c_int, i64, i32, vp, vp, vp, sz, vp],
+        "bkmoo_solve": [i32, i32, vp, ctypes.c_int, ctypes.POINTER(_Hparams), vp, vp, vp],
+        "bkmoo_combine": [i32, vpp, ctypes.c_int, i64, i32, vp, vp, vp, ctypes.c_int, vp, sz, vp],
+        "bkmoo_resolve": [i32, vpp, ctypes.c_int, i64, i32, vp, ctypes.c_int, ctypes.POINTER(_Hparams),
+                          vp, ctypes.c_int, vp, vp, vp, vp, sz, vp],
+        "bkmoo_read_device_error": [vp, ctypes.POINTER(u32), vp],
+        "bkmoo_set_grid_override": [i32],
+        "bkmoo_status_string": [ctypes.c_int],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_char_p if name == "bkmoo_status_string" else ctypes.c_int
+    return lib
+
+
+_lib = _load()
+
+EXPORTS = ("bkmoo_workspace_size", "bkmoo_gram", "bkmoo_solve", "bkmoo_combine", "bkmoo_resolve",
+           "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_status_string")
+
+
+def status_string(st: int) -> str:
+    return _lib.bkmoo_status_string(st).decode()
+
+
+def _check(st: int, what: str):
+    if st != 0:
+        raise BkmooError(f"{what}: {status_string(st)} ({st})")
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _torch_dt(code: int):
+    return torch.float32 if code == F32 else torch.bfloat16
+
+
+def _stream_ptr(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+Grads = Union[torch.Tensor, Sequence[torch.Tensor]]
+
+
+def _rows(grads: Grads):
+    """K row pointers (host array), dtype code, K, N, device."""
+    if isinstance(grads, torch.Tensor):
+        if grads.dim() != 2:
+            raise ValueError("grads must be [K, N] or a list of K 1-D tensors")
+        if not grads.is_contiguous():
+            raise ValueError("a [K, N] grads tensor must be contiguous")
+        rows = [grads[i] for i in range(grads.shape[0])]
+    else:
+        rows = list(grads)
+    if not rows:
+        raise ValueError("no gradient rows")
+    dt = _dt(rows[0])
+    n = rows[0].numel()
+    dev = rows[0].device
+    for r in rows:
+        if r.dtype != rows[0].dtype or r.numel() != n or r.device != dev or r.dim() != 1 \
+                or not r.is_contiguous():
+            raise ValueError("rows must be contiguous 1-D tensors of one dtype, length and device")
+        if dev.type != "cuda":
+            raise ValueError("gradient rows must be on a GPU")
+    arr = (ctypes.c_void_p * len(rows))(*[r.data_ptr() for r in rows])
+    return arr, dt, len(rows), n, dev, rows
+
+
+def _offsets(offsets: torch.Tensor, dev) -> torch.Tensor:
+    if offsets.dtype != torch.int64 or offsets.dim() != 1 or offsets.device != dev \
+            or not offsets.is_contiguous():
+        raise ValueError("bucket_offsets must be a contiguous int64 1-D tensor on the grads' device")
+    return offsets
+
+
+def _hparams(max_iter: int, cagrad_c: float, pcgrad_order: Optional[torch.Tensor], K: int, B: int):
+    ptr = None
+    if pcgrad_order is not None:
+        if pcgrad_order.dtype != torch.int8 or tuple(pcgrad_order.shape) != (B, K, K - 1) \
+                or not pcgrad_order.is_contiguous() or pcgrad_order.device.type != "cuda":
+            raise ValueError("pcgrad_order must be a contiguous int8 [B, K, K-1] GPU tensor")
+        ptr = pcgrad_order.data_ptr()
+    return _Hparams(int(max_iter), float(cagrad_c), ptr)
+
+
+def workspace_size(K: int, N: int, B: int, dtype) -> int:
+    code = dtype if isinstance(dtype, int) else (F32 if dtype in (torch.float32, "f32") else BF16)
+    out = ctypes.c_size_t(0)
+    _check(_lib.bkmoo_workspace_size(K, N, B, code, ctypes.byref(out)), "bkmoo_workspace_size")
+    return out.value
+
+
+def _workspace(ws: Optional[torch.Tensor], K, N, B, dt, dev) -> torch.Tensor:
+    need = workspace_size(K, N, B, dt)
+    if ws is None:
+        return torch.empty(need, dtype=torch.uint8, device=dev)
+    if ws.dtype != torch.uint8 or ws.device != dev or not ws.is_contiguous():
+        raise ValueError("workspace must be a contiguous uint8 tensor on the grads' device")
+    return ws
+
+
+def gram(grads: Grads, bucket_offsets: torch.Tensor, gram_out: Optional[torch.Tensor] = None,
+         workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Per-bucket Gram matrices, fp64 [B, K, K]."""
+    arr, dt, K, N, dev, _ = _rows(grads)
+    offs = _offsets(bucket_offsets, dev)
+    B = offs.numel() - 1
+    if gram_out is None:
+        gram_out = torch.empty((B, K, K), dtype=torch.float64, device=dev)
+    ws = _workspace(workspace, K, N, B, dt, dev)
+    _check(_lib.bkmoo_gram(K, arr, dt, N, B, offs.data_ptr(), gram_out.data_ptr(), ws.data_ptr(),
+                           ws.numel(), _stream_ptr(dev)), "bkmoo_gram")
+    return gram_out
+
+
+def solve(gram_in: torch.Tensor, method: str, max_iter: int = 20, cagrad_c: float = 0.5,
+          pcgrad_order: Optional[torch.Tensor] = None, weights: Optional[torch.Tensor] = None,
+          aux: Optional[torch.Tensor] = None):
+    """Per-bucket combine weights (fp32 [B, K]) and the method's variable (fp64 [B, K])."""
+    if gram_in.dtype != torch.float64 or gram_in.dim() != 3 or not gram_in.is_contiguous():
+        raise ValueError("gram must be a contiguous fp64 [B, K, K] tensor")
+    B, K, _ = gram_in.shape
+    dev = gram_in.device
+    if weights is None:
+        weights = torch.empty((B, K), dtype=torch.float32, device=dev)
+    if aux is None:
+        aux = torch.empty((B, K), dtype=torch.float64, device=dev)
+    hp = _hparams(max_iter, cagrad_c, pcgrad_order, K, B)
+    _check(_lib.bkmoo_solve(K, B, gram_in.data_ptr(), METHODS[method], ctypes.byref(hp),
+                            weights.data_ptr(), aux.data_ptr(), _stream_ptr(dev)), "bkmoo_solve")
+    return weights, aux
+
+
+def combine(grads: Grads, bucket_offsets: torch.Tensor, weights: torch.Tensor,
+            out: Optional[torch.Tensor] = None, out_dtype=None,
+            workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The concatenated bucket updates, N elements of out_dtype (default: input dtype)."""
+    arr, dt, K, N, dev, _ = _rows(grads)
+    offs = _offsets(bucket_offsets, dev)
+    B = offs.numel() - 1
+    if weights.dtype != torch.float32 or tuple(weights.shape) != (B, K) or not weights.is_contiguous():
+        raise ValueError("weights must be a contiguous fp32 [B, K] tensor")
+    if out is None:
+        out = torch.empty(N, dtype=out_dtype or _torch_dt(dt), device=dev)
+    odt = _dt(out)
+    ws = _workspace(workspace, K, N, B, dt, dev)
+    _check(_lib.bkmoo_combine(K, arr, dt, N, B, offs.data_ptr(), weights.data_ptr(), out.data_ptr(),
+                              odt, ws.data_ptr(), ws.numel(), _stream_ptr(dev)), "bkmoo_combine")
+    return out
+
+
+def resolve(grads: Grads, bucket_offsets: torch.Tensor, method: str, max_iter: int = 20,
+            cagrad_c: float = 0.5, pcgrad_order: Optional[torch.Tensor] = None,
+            out: Optional[torch.Tensor] = None, out_dtype=None,
+            gram_out: Optional[torch.Tensor] = None, weights: Optional[torch.Tensor] = None,
+            aux: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    """Gram -> solve -> combine on the current stream.  Returns `out`; gram,
+    weights and aux are written to the tensors passed (if any)."""
+    arr, dt, K, N, dev, _ = _rows(grads)
+    offs = _offsets(bucket_offsets, dev)
+    B = offs.numel() - 1
+    if out is None:
+        out = torch.empty(N, dtype=out_dtype or _torch_dt(dt), device=dev)
+    odt = _dt(out)
+    ws = _workspace(workspace, K, N, B, dt, dev)
+    hp = _hparams(max_iter, cagrad_c, pcgrad_order, K, B)
+
+    def ptr(t, shape, dtype):
+        if t is None:
+            return None
+        if t.dtype != dtype or tuple(t.shape) != shape or not t.is_contiguous() or t.device != dev:
+            raise ValueError(f"expected a contiguous {dtype} {shape} tensor")
+        return t.data_ptr()
+
+    _check(_lib.bkmoo_resolve(K, arr, dt, N, B, offs.data_ptr(), METHODS[method], ctypes.byref(hp),
+                              out.data_ptr(), odt, ptr(gram_out, (B, K, K), torch.float64),
+                              ptr(weights, (B, K), torch.float32), ptr(aux, (B, K), torch.float64),
+                              ws.data_ptr(), ws.numel(), _stream_ptr(dev)), "bkmoo_resolve")
+    return out
+
+
+def read_device_error(workspace: torch.Tensor) -> int:
+    v = ctypes.c_uint32(0)
+    _check(_lib.bkmoo_read_device_error(workspace.data_ptr(), ctypes.byref(v),
+                                        _stream_ptr(workspace.device)), "bkmoo_read_device_error")
+    return v.value
+
+
+def set_grid_override(workgroups: int):
+    _check(_lib.bkmoo_set_grid_override(int(workgroups)), "bkmoo_set_grid_override")

@@ -1,0 +1,237 @@
+// C ABI of libbkmoo: argument checks, workspace carving and stream-ordered
+// launches of schedule -> Gram -> solve -> combine.  Nothing here allocates,
+// frees or synchronises (except bkmoo_read_device_error, a diagnostic).
+#include <atomic>
+#include <mutex>
+
+#include "bkmoo.h"
+#include "internal.h"
+
+namespace bkmoo {
+
+namespace {
+
+std::atomic<int> g_grid_override{0};
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cu_count[kMaxDevices];
+
+bool valid_dtype(int dt) { return dt == BKMOO_F32 || dt == BKMOO_BF16; }
+
+// Shapes shared by gram / combine / resolve.
+bkmoo_status check_shape(int32_t K, int64_t N, int32_t B, int dt) {
+  if (K < kMinK || N < 0 || B < 1 || !valid_dtype(dt)) return BKMOO_EINVAL;
+  if (K > kMaxK) return BKMOO_EUNSUPPORTED;
+  return BKMOO_OK;
+}
+
+// Row pointers: non-null, naturally aligned.  128-bit loads need every row
+// at the same 16-byte phase; `shift` is then the first element index whose
+// address is 16-byte aligned, modulo the vector width.
+bkmoo_status check_rows(int32_t K, const void *const *grads, int dt, int64_t N, int *shift,
+                        bool *vec) {
+  if (!grads) return BKMOO_EINVAL;
+  const uintptr_t eb = (uintptr_t)elem_bytes(dt);
+  const uintptr_t a0 = (uintptr_t)grads[0];
+  bool same_phase = true;
+  for (int i = 0; i < K; ++i) {
+    const uintptr_t a = (uintptr_t)grads[i];
+    if ((N > 0 && a == 0) || a % eb != 0) return BKMOO_EINVAL;
+    if (a % 16 != a0 % 16) same_phase = false;
+  }
+  *shift = (int)(((16 - a0 % 16) % 16) / eb);
+  *vec = same_phase;
+  return BKMOO_OK;
+}
+
+bool overlaps(uintptr_t a, size_t na, uintptr_t b, size_t nb) { return a < b + nb && b < a + na; }
+
+bkmoo_status check_out(int32_t K, const void *const *grads, int dt, int64_t N, const void *out,
+                       int out_dt, int shift, bool *vec) {
+  if (!valid_dtype(out_dt)) return BKMOO_EINVAL;
+  const uintptr_t o = (uintptr_t)out;
+  const uintptr_t eo = (uintptr_t)elem_bytes(out_dt);
+  if ((N > 0 && o == 0) || o % eo != 0) return BKMOO_EINVAL;
+  const size_t nbo = (size_t)N * eo, nbi = (size_t)N * elem_bytes(dt);
+  for (int i = 0; i < K; ++i) {
+    const uintptr_t r = (uintptr_t)grads[i];
+    if (r == o && out_dt == dt) continue;  // exact in-place update of one row
+    if (N > 0 && overlaps(o, nbo, r, nbi)) return BKMOO_EINVAL;
+  }
+  // vector stores: V outputs at out + (shift + m V) * s_out, 8 or 16 bytes wide
+  const uintptr_t width = (uintptr_t)vec_elems(dt) * eo < 16 ? (uintptr_t)vec_elems(dt) * eo : 16;
+  if ((o + (uintptr_t)shift * eo) % width != 0) *vec = false;
+  return BKMOO_OK;
+}
+
+bkmoo_status check_hparams(int method, const bkmoo_hparams *hp) {
+  if (method < BKMOO_MGDA || method > BKMOO_MEAN) return BKMOO_EINVAL;
+  if (method == BKMOO_MEAN) return BKMOO_OK;
+  if (!hp) return BKMOO_EINVAL;
+  if (method != BKMOO_PCGRAD && (hp->max_iter < 0 || hp->max_iter > 1000000)) return BKMOO_EINVAL;
+  if (method == BKMOO_CAGRAD && !(hp->cagrad_c >= 0.0 && hp->cagrad_c < 1.0)) return BKMOO_EINVAL;
+  return BKMOO_OK;
+}
+
+bkmoo_status hip_status(hipError_t e) { return e == hipSuccess ? BKMOO_OK : BKMOO_EHIP; }
+
+struct Carved {
+  uint32_t *err;
+  int64_t *chunk_start;
+  double *gram;
+  float *weights;
+  double *partials;
+};
+
+Carved carve(void *ws, const Layout &L) {
+  char *base = static_cast<char *>(ws);
+  return Carved{reinterpret_cast<uint32_t *>(base + L.err),
+                reinterpret_cast<int64_t *>(base + L.chunk_start),
+                reinterpret_cast<double *>(base + L.gram), reinterpret_cast<float *>(base + L.weights),
+                reinterpret_cast<double *>(base + L.partials)};
+}
+
+}  // namespace
+
+int device_cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 1;
+  if (dev < kMaxDevices) {
+    const int cached = g_cu_count[dev].load(std::memory_order_relaxed);
+    if (cached > 0) return cached;
+  }
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+    n = 1;
+  if (dev < kMaxDevices) g_cu_count[dev].store(n, std::memory_order_relaxed);
+  return n;
+}
+
+}  // namespace bkmoo
+
+using namespace bkmoo;
+
+extern "C" {
+
+bkmoo_status bkmoo_workspace_size(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt, size_t *bytes) {
+  if (!bytes) return BKMOO_EINVAL;
+  const bkmoo_status st = check_shape(K, N, B, dt);
+  if (st != BKMOO_OK) return st;
+  *bytes = layout(K, N, B, dt).total;
+  return BKMOO_OK;
+}
+
+bkmoo_status bkmoo_gram(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
+                        const int64_t *bucket_offsets, double *gram, void *workspace,
+                        size_t ws_bytes, hipStream_t stream) {
+  bkmoo_status st = check_shape(K, N, B, dt);
+  if (st != BKMOO_OK) return st;
+  int shift = 0;
+  bool vec = false;
+  if ((st = check_rows(K, grads, dt, N, &shift, &vec)) != BKMOO_OK) return st;
+  if (!bucket_offsets || !gram || !workspace) return BKMOO_EINVAL;
+  const Layout L = layout(K, N, B, dt);
+  if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
+  const Carved w = carve(workspace, L);
+  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err, stream);
+  if (e != hipSuccess) return BKMOO_EHIP;
+  const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec,
+                     g_grid_override.load()};
+  return hip_status(launch_gram(a, w.partials, gram, stream));
+}
+
+bkmoo_status bkmoo_solve(int32_t K, int32_t B, const double *gram, bkmoo_method method,
+                         const bkmoo_hparams *hp, float *weights, double *aux, hipStream_t stream) {
+  if (K < kMinK || B < 1) return BKMOO_EINVAL;
+  if (K > kMaxK) return BKMOO_EUNSUPPORTED;
+  if (!gram || !weights) return BKMOO_EINVAL;
+  const bkmoo_status st = check_hparams(method, hp);
+  if (st != BKMOO_OK) return st;
+  const int iters = hp ? hp->max_iter : 0;
+  const double c = hp ? hp->cagrad_c : 0.0;
+  const int8_t *order = hp ? hp->pcgrad_order : nullptr;
+  return hip_status(launch_solve(K, B, gram, (int)method, iters, c, order, weights, aux, stream));
+}
+
+bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
+                           const int64_t *bucket_offsets, const float *weights, void *out,
+                           bkmoo_dtype out_dt, void *workspace, size_t ws_bytes, hipStream_t stream) {
+  bkmoo_status st = check_shape(K, N, B, dt);
+  if (st != BKMOO_OK) return st;
+  int shift = 0;
+  bool vec = false;
+  if ((st = check_rows(K, grads, dt, N, &shift, &vec)) != BKMOO_OK) return st;
+  if ((st = check_out(K, grads, dt, N, out, out_dt, shift, &vec)) != BKMOO_OK) return st;
+  if (!bucket_offsets || !weights || !workspace) return BKMOO_EINVAL;
+  const Layout L = layout(K, N, B, dt);
+  if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
+  const Carved w = carve(workspace, L);
+  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err, stream);
+  if (e != hipSuccess) return BKMOO_EHIP;
+  const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec,
+                     g_grid_override.load()};
+  return hip_status(launch_combine(a, weights, out, (int)out_dt, stream));
+}
+
+bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
+                           const int64_t *bucket_offsets, bkmoo_method method,
+                           const bkmoo_hparams *hp, void *out, bkmoo_dtype out_dt, double *gram,
+                           float *weights, double *aux, void *workspace, size_t ws_bytes,
+                           hipStream_t stream) {
+  bkmoo_status st = check_shape(K, N, B, dt);
+  if (st != BKMOO_OK) return st;
+  int shift = 0;
+  bool vec_in = false;
+  if ((st = check_rows(K, grads, dt, N, &shift, &vec_in)) != BKMOO_OK) return st;
+  bool vec_out = vec_in;
+  if ((st = check_out(K, grads, dt, N, out, out_dt, shift, &vec_out)) != BKMOO_OK) return st;
+  if ((st = check_hparams(method, hp)) != BKMOO_OK) return st;
+  if (!bucket_offsets || !workspace) return BKMOO_EINVAL;
+  const Layout L = layout(K, N, B, dt);
+  if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
+  const Carved w = carve(workspace, L);
+  double *G = gram ? gram : w.gram;
+  float *W = weights ? weights : w.weights;
+
+  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err, stream);
+  if (e != hipSuccess) return BKMOO_EHIP;
+  StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec_in,
+               g_grid_override.load()};
+  if ((e = launch_gram(a, w.partials, G, stream)) != hipSuccess) return BKMOO_EHIP;
+  const int iters = hp ? hp->max_iter : 0;
+  const double c = hp ? hp->cagrad_c : 0.0;
+  const int8_t *order = hp ? hp->pcgrad_order : nullptr;
+  if ((e = launch_solve(K, B, G, (int)method, iters, c, order, W, aux, stream)) != hipSuccess)
+    return BKMOO_EHIP;
+  a.vec = vec_out;
+  return hip_status(launch_combine(a, W, out, (int)out_dt, stream));
+}
+
+bkmoo_status bkmoo_read_device_error(const void *workspace, uint32_t *err, hipStream_t stream) {
+  if (!workspace || !err) return BKMOO_EINVAL;
+  uint32_t v = 0;
+  if (hipMemcpyAsync(&v, workspace, sizeof(v), hipMemcpyDeviceToHost, stream) != hipSuccess)
+    return BKMOO_EHIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return BKMOO_EHIP;
+  *err = v;
+  return BKMOO_OK;
+}
+
+bkmoo_status bkmoo_set_grid_override(int32_t workgroups) {
+  if (workgroups < 0) return BKMOO_EINVAL;
+  g_grid_override.store(workgroups);
+  return BKMOO_OK;
+}
+
+const char *bkmoo_status_string(bkmoo_status st) {
+  switch (st) {
+    case BKMOO_OK: return "BKMOO_OK";
+    case BKMOO_EINVAL: return "BKMOO_EINVAL: invalid argument";
+    case BKMOO_EUNSUPPORTED: return "BKMOO_EUNSUPPORTED: unsupported configuration";
+    case BKMOO_EWORKSPACE: return "BKMOO_EWORKSPACE: workspace too small";
+    case BKMOO_EHIP: return "BKMOO_EHIP: HIP launch or runtime failure";
+    default: return "BKMOO: unknown status";
+  }
+}
+
+}  // extern "C"

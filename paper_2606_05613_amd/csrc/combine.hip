@@ -1,0 +1,218 @@
+// Pass 2: the resolved bucket updates d[o_b:o_{b+1}] = sum_i w_{b,i} x_i,
+// concatenated over buckets (Algorithm 1: the per-strategy d_(k), then
+// d = [d_(1), ..., d_(K)]).
+//
+// Bandwidth-bound: K*N*s bytes read, N*s_out written, 2K flops per
+// element.  Same chunking and 128-bit non-temporal loads as the Gram pass;
+// the K weights of a chunk's bucket are wave-uniform scalars.
+//
+// Arithmetic.  For an fp32 output the sum is an fp32 FMA chain in task
+// order.  For a bf16 output that is not enough: with bf16 inputs the exact
+// sum of w_i x_i often lies within an fp32 rounding error of a bf16 tie
+// (e.g. weights of 1/K), and an fp32 chain then rounds the wrong way on a
+// few percent of elements.  So the bf16 path accumulates in fp64, where
+// every product of an fp32 weight and an fp32/bf16 input is exact, and
+// rounds once: fp64 -> fp32 with round-to-odd, then RNE to bf16.  Rounding
+// to odd into a format with at least two more significand bits than the
+// target makes the second rounding the correct single rounding.
+#include "stream_common.h"
+
+namespace bkmoo {
+
+namespace {
+
+template <int ODT>
+__device__ __forceinline__ void store_elem(void *out, int64_t n, float y) {
+  if constexpr (ODT == F32) {
+    static_cast<float *>(out)[n] = y;
+  } else {
+    static_cast<__bf16 *>(out)[n] = (__bf16)y;
+  }
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Store V results (V = 4 or 8) at out + first*s_out, 16-byte or 8-byte wide.
+template <int ODT, int V>
+__device__ __forceinline__ void store_vec(void *out, int64_t first, const float *y) {
+  if constexpr (ODT == F32) {
+    u32x4 *p = reinterpret_cast<u32x4 *>(static_cast<float *>(out) + first);
+#pragma unroll
+    for (int q = 0; q < V / 4; ++q) {
+      u32x4 v = {__float_as_uint(y[4 * q]), __float_as_uint(y[4 * q + 1]),
+                 __float_as_uint(y[4 * q + 2]), __float_as_uint(y[4 * q + 3])};
+      __builtin_nontemporal_store(v, p + q);
+    }
+  } else if constexpr (V == 8) {
+    u32x4 v = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
+               pack_bf16x2(y[6], y[7])};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(static_cast<__bf16 *>(out) + first));
+  } else {
+    u32x2 v = {pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3])};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x2 *>(static_cast<__bf16 *>(out) + first));
+  }
+}
+
+// fp64 -> fp32 rounding to odd: truncate toward zero and, if anything was
+// dropped, set the last significand bit.  NaN stays NaN; values beyond the
+// fp32 range become +-FLT_MAX with the odd bit set (which a bf16 RNE then
+// sends to infinity, as the exact value would).
+__device__ __forceinline__ float f32_round_odd(double d) {
+  float f = (float)d;
+  const double back = (double)f;
+  if (back != d) {
+    uint32_t u = __float_as_uint(f);
+    if (fabs(back) > fabs(d)) u -= 1u;
+    f = __uint_as_float(u | 1u);
+  }
+  return f;
+}
+
+// sum_i w_i x_i for the output type ODT: an fp32 FMA chain for fp32
+// outputs; for bf16 outputs an fp64 chain rounded to odd into fp32 (the
+// store then rounds to nearest even).
+template <int K, int ODT>
+__device__ __forceinline__ float wsum(const float *w, const float *x) {
+  if constexpr (ODT == F32) {
+    float y = w[0] * x[0];
+#pragma unroll
+    for (int i = 1; i < K; ++i) y = __builtin_fmaf(w[i], x[i], y);
+    return y;
+  } else {
+    double y = (double)w[0] * (double)x[0];
+#pragma unroll
+    for (int i = 1; i < K; ++i) y = __builtin_fma((double)w[i], (double)x[i], y);
+    return f32_round_odd(y);
+  }
+}
+
+template <int K, int DT, int ODT>
+__global__ __launch_bounds__(kThreads) void combine_kernel(
+    Rows<K> rows, const int64_t *__restrict__ offs, const int64_t *__restrict__ cs, int B,
+    int shift, int vec, const float *__restrict__ weights, void *out) {
+  constexpr int V = vec_elems(DT);
+  constexpr int R = rows_per_thread(K);
+  constexpr int U = iters_per_chunk(K);
+  constexpr int64_t C = chunk_elems(K, DT);
+  constexpr int EB = elem_bytes(DT);
+
+  int64_t c, cend;
+  my_chunks(cs[B], c, cend);
+  if (c >= cend) return;
+  int b = find_bucket(cs, B, c);
+  const int tid = threadIdx.x;
+
+  for (; c < cend; ++c) {
+    while (cs[b + 1] <= c) ++b;
+    const int64_t lo = offs[b] + (c - cs[b]) * C;
+    const int64_t hi = lo + C < offs[b + 1] ? lo + C : offs[b + 1];
+    float w[K];
+#pragma unroll
+    for (int i = 0; i < K; ++i) w[i] = weights[(int64_t)b * K + i];
+
+    if (vec) {
+      const Split<V> sp(lo, hi, shift);
+      if (tid < sp.nh + sp.nt) {
+        const int64_t n = tid < sp.nh ? lo + tid : sp.hi_a + (tid - sp.nh);
+        float x[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) x[i] = load_elem<DT>(rows.p[i], n);
+        store_elem<ODT>(out, n, wsum<K, ODT>(w, x));
+      }
+#pragma unroll 2
+      for (int u = 0; u < U; ++u) {
+        const int vb = u * kThreads * R + tid;
+        u32x4 buf[R][K];
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const int v = vb + r * kThreads;
+          if (v < sp.nv) {
+#pragma unroll
+            for (int i = 0; i < K; ++i)
+              buf[r][i] = stream_load(static_cast<const char *>(rows.p[i]) + sp.lo_a * EB, v);
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          const int v = vb + r * kThreads;
+          if (v < sp.nv) {
+            float x[K][V];
+#pragma unroll
+            for (int i = 0; i < K; ++i) decode<DT>(buf[r][i], x[i]);
+            float y[V];
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+              float xe[K];
+#pragma unroll
+              for (int i = 0; i < K; ++i) xe[i] = x[i][e];
+              y[e] = wsum<K, ODT>(w, xe);
+            }
+            store_vec<ODT, V>(out, sp.lo_a + (int64_t)v * V, y);
+          }
+        }
+      }
+    } else {
+      for (int64_t n = lo + tid; n < hi; n += kThreads) {
+        float x[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) x[i] = load_elem<DT>(rows.p[i], n);
+        store_elem<ODT>(out, n, wsum<K, ODT>(w, x));
+      }
+    }
+  }
+}
+
+template <int K, int DT, int ODT>
+hipError_t launch_combine_t(const StreamArgs &a, const float *weights, void *out, hipStream_t s) {
+  Rows<K> rows;
+  for (int i = 0; i < K; ++i) rows.p[i] = a.rows[i];
+  auto kern = combine_kernel<K, DT, ODT>;
+  const int64_t C = chunk_elems(K, DT);
+  const int64_t cap = (a.N + C - 1) / C + a.B;
+  static const int occ = occupancy(kern);
+  int64_t grid = a.grid > 0 ? a.grid : (int64_t)device_cu_count() * occ;
+  if (grid > cap) grid = cap;
+  if (grid < 1) grid = 1;
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), 0, s, rows, a.offsets,
+                     a.chunk_start, a.B, a.shift, a.vec ? 1 : 0, weights, out);
+  return hipGetLastError();
+}
+
+template <int DT, int ODT>
+hipError_t dispatch_combine(const StreamArgs &a, const float *w, void *out, hipStream_t s) {
+  switch (a.K) {
+    case 2: return launch_combine_t<2, DT, ODT>(a, w, out, s);
+    case 3: return launch_combine_t<3, DT, ODT>(a, w, out, s);
+    case 4: return launch_combine_t<4, DT, ODT>(a, w, out, s);
+    case 5: return launch_combine_t<5, DT, ODT>(a, w, out, s);
+    case 6: return launch_combine_t<6, DT, ODT>(a, w, out, s);
+    case 7: return launch_combine_t<7, DT, ODT>(a, w, out, s);
+    case 8: return launch_combine_t<8, DT, ODT>(a, w, out, s);
+    case 9: return launch_combine_t<9, DT, ODT>(a, w, out, s);
+    case 10: return launch_combine_t<10, DT, ODT>(a, w, out, s);
+    case 11: return launch_combine_t<11, DT, ODT>(a, w, out, s);
+    case 12: return launch_combine_t<12, DT, ODT>(a, w, out, s);
+    case 13: return launch_combine_t<13, DT, ODT>(a, w, out, s);
+    case 14: return launch_combine_t<14, DT, ODT>(a, w, out, s);
+    case 15: return launch_combine_t<15, DT, ODT>(a, w, out, s);
+    case 16: return launch_combine_t<16, DT, ODT>(a, w, out, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_combine(const StreamArgs &a, const float *weights, void *out, int out_dt,
+                          hipStream_t s) {
+  if (a.dt == F32)
+    return out_dt == F32 ? dispatch_combine<F32, F32>(a, weights, out, s)
+                         : dispatch_combine<F32, BF16>(a, weights, out, s);
+  return out_dt == F32 ? dispatch_combine<BF16, F32>(a, weights, out, s)
+                       : dispatch_combine<BF16, BF16>(a, weights, out, s);
+}
+
+}  // namespace bkmoo

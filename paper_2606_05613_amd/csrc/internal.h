@@ -1,0 +1,107 @@
+// Internal declarations shared by the bkmoo translation units (not installed).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace bkmoo {
+
+constexpr int kMinK = 2;
+constexpr int kMaxK = 16;
+constexpr int kThreads = 256;          // streaming kernels: 4 wavefronts of 64
+constexpr int kWave = 64;
+
+enum Dtype : int { F32 = 0, BF16 = 1 };
+
+// Vectors of 16 bytes: 4 fp32 or 8 bf16 elements.
+constexpr int vec_elems(int dt) { return dt == F32 ? 4 : 8; }
+constexpr int elem_bytes(int dt) { return dt == F32 ? 4 : 2; }
+
+// 16-byte vectors each thread loads per task row and iteration, and
+// iterations per chunk.  K * R bounds the registers holding loaded data
+// (4 per vector) next to K(K+1)/2 fp32 accumulators; occupancy (several
+// wavefronts per SIMD) supplies the rest of the memory-level parallelism.
+constexpr int rows_per_thread(int K) { return K <= 8 ? 2 : 1; }
+constexpr int iters_per_chunk(int K) { return K <= 8 ? 8 : 16; }
+
+// A chunk is the unit of streaming work: U iterations of kThreads * R
+// vectors.  Chunks never straddle buckets, so bucket b holds ceil(n_b / C)
+// chunks.  Each thread accumulates R * U * V elements of a chunk in fp32.
+constexpr int64_t chunk_elems(int K, int dt) {
+  return (int64_t)kThreads * rows_per_thread(K) * iters_per_chunk(K) * vec_elems(dt);
+}
+
+constexpr int pairs(int K) { return K * (K + 1) / 2; }
+
+// Workspace layout (every region 256-byte aligned):
+//   [0, 256)            header: uint32 error word at byte 0
+//   chunk_start         int64 [B + 1]     (prefix sum of chunks per bucket)
+//   gram                fp64  [B][K][K]   (used when the caller passes none)
+//   weights             fp32  [B][K]      (used when the caller passes none)
+//   partials            fp64  [cap][P]    cap = ceil(N / C) + B
+struct Layout {
+  size_t err, chunk_start, gram, weights, partials, total;
+  int64_t cap_chunks;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline Layout layout(int K, int64_t N, int B, int dt) {
+  Layout L;
+  const int64_t C = chunk_elems(K, dt);
+  L.cap_chunks = (N + C - 1) / C + B;
+  size_t o = 0;
+  L.err = o;            o += 256;
+  L.chunk_start = o;    o = align256(o + sizeof(int64_t) * (size_t)(B + 1));
+  L.gram = o;           o = align256(o + sizeof(double) * (size_t)B * K * K);
+  L.weights = o;        o = align256(o + sizeof(float) * (size_t)B * K);
+  L.partials = o;       o = align256(o + sizeof(double) * (size_t)L.cap_chunks * pairs(K));
+  L.total = o;
+  return L;
+}
+
+constexpr uint32_t kErrOffsets = 0x1u;
+
+// Pointers of the K task rows, passed by value as kernel arguments.
+template <int K>
+struct Rows {
+  const void *p[K];
+};
+
+// ---- launchers (host) -------------------------------------------------------
+
+struct StreamArgs {
+  int K;
+  int dt;                      // input dtype
+  const void *const *rows;     // host array of K device pointers
+  int64_t N;
+  int B;
+  const int64_t *offsets;      // device [B+1]
+  const int64_t *chunk_start;  // device [B+1] (from the schedule kernel)
+  const uint32_t *err;         // device error word
+  int shift;                   // rows are 16-byte aligned at element n = shift (mod V)
+  bool vec;                    // 128-bit path allowed
+  int grid;                    // workgroups (0: automatic)
+};
+
+hipError_t launch_schedule(const int64_t *offsets, int B, int64_t N, int64_t C, int64_t *chunk_start,
+                           uint32_t *err, hipStream_t s);
+hipError_t launch_gram(const StreamArgs &a, double *partials, double *gram, hipStream_t s);
+hipError_t launch_solve(int K, int B, const double *gram, int method, int max_iter, double c,
+                        const int8_t *order, float *weights, double *aux, hipStream_t s);
+hipError_t launch_combine(const StreamArgs &a, const float *weights, void *out, int out_dt,
+                          hipStream_t s);
+
+int device_cu_count();
+
+// Resident workgroups of kThreads per CU for a kernel (at least 1).
+template <typename Kern>
+int occupancy(Kern kern) {
+  int occ = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, kThreads, 0) != hipSuccess || occ < 1)
+    occ = 1;
+  return occ;
+}
+
+}  // namespace bkmoo

@@ -1,0 +1,68 @@
+// Bucket schedule: validates the bucket offsets and cuts every bucket into
+// chunks of C elements that never straddle a bucket boundary (the partition
+// of the parameter vector into disjoint contiguous buckets, Section 3.2).
+#include "internal.h"
+
+namespace bkmoo {
+
+namespace {
+
+constexpr int kSchedThreads = 1024;
+
+// One workgroup.  chunk_start[b] = sum_{b' < b} ceil(n_b' / C); on invalid
+// offsets every entry is 0 (so no chunk is processed) and the error word
+// gets kErrOffsets.  Otherwise the error word is cleared.
+__global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
+    const int64_t *__restrict__ offs, int B, int64_t N, int64_t C, int64_t *__restrict__ cs,
+    uint32_t *__restrict__ err) {
+  __shared__ int bad;
+  __shared__ int64_t scan[kSchedThreads];
+  __shared__ int64_t carry;
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    bad = (offs[0] != 0 || offs[B] != N) ? 1 : 0;
+    carry = 0;
+  }
+  __syncthreads();
+  for (int b = tid; b < B; b += kSchedThreads)
+    if (offs[b + 1] < offs[b]) bad = 1;
+  __syncthreads();
+  if (bad) {
+    for (int b = tid; b <= B; b += kSchedThreads) cs[b] = 0;
+    if (tid == 0) *err = kErrOffsets;
+    return;
+  }
+  for (int base = 0; base < B; base += kSchedThreads) {
+    const int b = base + tid;
+    const int64_t n = b < B ? offs[b + 1] - offs[b] : 0;
+    const int64_t cnt = (n + C - 1) / C;
+    scan[tid] = cnt;
+    __syncthreads();
+    // Hillis-Steele inclusive scan over the tile
+    for (int d = 1; d < kSchedThreads; d <<= 1) {
+      const int64_t add = tid >= d ? scan[tid - d] : 0;
+      __syncthreads();
+      scan[tid] += add;
+      __syncthreads();
+    }
+    if (b < B) cs[b] = carry + scan[tid] - cnt;
+    __syncthreads();
+    if (tid == kSchedThreads - 1) carry += scan[tid];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    cs[B] = carry;
+    *err = 0u;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_schedule(const int64_t *offsets, int B, int64_t N, int64_t C, int64_t *chunk_start,
+                           uint32_t *err, hipStream_t s) {
+  hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(kSchedThreads), 0, s, offsets, B, N, C,
+                     chunk_start, err);
+  return hipGetLastError();
+}
+
+}  // namespace bkmoo
