@@ -1,0 +1,214 @@
+"""Benchmark of the bucket-level resolve step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one pass of the whole hot path over the workload's gradients,
+already resident in HBM: the per-bucket Gram matrices, the per-bucket solve
+and the combined update (the three stage entry points in stream order; the
+same kernels bkmoo_resolve launches, with identical results).  The default
+workload is the Llama-3-8B-shaped K=4 bf16 MGDA (Frank-Wolfe, 20 iterations)
+case with 25 MiB buckets.  Prints ONE JSON line.
+
+Reported next to the throughput:
+  roofline     the longest kernel of a step (HBM-bound), timed with HIP
+               events on its launch stream inside the timed region:
+               algorithmic bytes per launch / average launch duration,
+               against MI355X's 8 TB/s; `traffic` comes from the committed
+               rocprofv3 counter summary when it matches the current kernel
+               source, else null;
+  cpu_baseline the float64 oracle on a bounded prefix of the same buckets,
+               on this host's cores.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0
+METRIC = "resolved grad elems/s (K·N/s) + achieved HBM GB/s vs peak, K=4 MGDA 8B-shape"
+DEFAULT_WORKLOAD = "llama3-8b-k4-mgda-bf16"
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_05613_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    rocprofv3 counter summary, if it was taken on the current source."""
+    path = os.path.join(PROFILE_DIR, f"{kernel}_{workload}_pmc.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    sha = re.search(r"source_sha:\s*(\w+)", text)
+    val = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not sha or not val or sha.group(1) != kernel_source_sha():
+        return None
+    return float(val.group(1))
+
+
+def cpu_baseline(wl, grads, target_s: float):
+    """The oracle, as it stands, on a prefix of the workload's buckets."""
+    import numpy as np
+    import oracle
+    from synth import host_rows
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    offs = wl.offsets()
+    orders = wl.orders() if wl.method == "pcgrad" else None
+    done_elems, spent, nb = 0, 0.0, 0
+    while nb < wl.B and spent < target_s:
+        lo, hi = int(offs[nb]), int(offs[nb + 1])
+        rows = host_rows(grads, lo, hi)                       # D2H copy, not timed
+        t0 = time.perf_counter()
+        oracle.resolve(rows, np.array([0, hi - lo]), wl.method, max_iter=wl.max_iter,
+                       cagrad_c=wl.cagrad_c, orders=None if orders is None else orders[nb:nb + 1])
+        spent += time.perf_counter() - t0
+        done_elems += hi - lo
+        nb += 1
+    return {"value": wl.K * done_elems / spent, "unit": "elem/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {nb} of {wl.B} buckets ({wl.K}x{done_elems} elements), oracle.resolve "
+                      f"end to end (Gram, {wl.method}, combine, rounding), {spent:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): this build has no multi-GPU "
+              "path; the bucket-level resolve shards by buckets and bucket slices, which is described "
+              "but not built.", flush=True)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_05613_amd import bkmoo
+    from synth import WORKLOADS, fill_grads
+
+    wl = WORKLOADS[args.workload]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    K, N, B, s = wl.K, wl.N, wl.B, wl.elem_bytes
+    log(f"workload {wl.name}: K={K} N={N} B={B} {wl.dtype} {wl.method}; generating "
+        f"{K * N * s / 1e9:.1f} GB of gradients on {torch.cuda.get_device_name(dev)}")
+    t0 = time.time()
+    last = [t0]
+
+    def progress(b):
+        if time.time() - last[0] > 5:
+            last[0] = time.time()
+            log(f"  generated bucket {b + 1}/{B}")
+
+    grads = fill_grads(wl, device=dev, progress=progress)
+    torch.cuda.synchronize()
+    log(f"generated in {time.time() - t0:.1f} s")
+    offs = torch.from_numpy(wl.offsets()).to(dev)
+    order = torch.from_numpy(wl.orders()).to(dev) if wl.method == "pcgrad" else None
+    out = torch.empty(N, dtype=grads.dtype, device=dev)
+    ws = torch.empty(bkmoo.workspace_size(K, N, B, wl.dtype), dtype=torch.uint8, device=dev)
+    G = torch.empty((B, K, K), dtype=torch.float64, device=dev)
+    W = torch.empty((B, K), dtype=torch.float32, device=dev)
+    A = torch.empty((B, K), dtype=torch.float64, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        bkmoo.gram(grads, offs, gram_out=G, workspace=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        bkmoo.solve(G, wl.method, wl.max_iter, wl.cagrad_c, pcgrad_order=order, weights=W, aux=A)
+        if ev is not None:
+            ev[2].record(stream)
+        bkmoo.combine(grads, offs, W, out=out, workspace=ws)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for i in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if bkmoo.read_device_error(ws) != 0:
+        raise RuntimeError("device reported invalid bucket offsets")
+    log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_start
+    ms_step = t_wall * 1e3 / args.steps
+    st = {"gram": 0.0, "solve": 0.0, "combine": 0.0}
+    for ev in events:
+        st["gram"] += ev[0].elapsed_time(ev[1]) / args.steps
+        st["solve"] += ev[1].elapsed_time(ev[2]) / args.steps
+        st["combine"] += ev[2].elapsed_time(ev[3]) / args.steps
+    log(f"{ms_step:.3f} ms/step; stages (ms) " + ", ".join(f"{k} {v:.3f}" for k, v in st.items()))
+
+    # dominant kernel: the longer of the two streaming passes
+    if st["combine"] >= st["gram"]:
+        kname, kbytes, kms = "combine", (K + 1) * s * N, st["combine"]
+    else:
+        kname, kbytes, kms = "gram", K * s * N, st["gram"]
+    achieved = kbytes / (kms / 1e3) / 1e9
+    traffic = committed_traffic(wl.name, kname)
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic, "kernel": kname,
+            "algorithmic_bytes_per_launch": kbytes, "avg_launch_ms": round(kms, 4)}
+    result = {
+        "metric": METRIC,
+        "value": K * N / (ms_step / 1e3),
+        "unit": "elem/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "K": K, "N": N, "B": B, "bucket_elems": wl.bucket_elems,
+                   "method": wl.method, "max_iter": wl.max_iter, "cagrad_c": wl.cagrad_c},
+        "stages_ms": {k: round(v, 4) for k, v in st.items()},
+        "resolve_algorithmic_GBps": round((2 * K + 1) * s * N / (ms_step / 1e3) / 1e9, 1),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log(f"oracle CPU baseline, ~{args.cpu_seconds:.0f} s")
+        result["cpu_baseline"] = cpu_baseline(wl, grads, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
