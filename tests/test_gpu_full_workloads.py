@@ -1,0 +1,118 @@
+"""Parity at the full sizes of the five model-shaped workloads, in the launch
+configuration the benchmark times (automatic grid).
+
+At these sizes the oracle cannot redo everything, so each workload checks:
+* every bucket: the oracle's solver run on the GPU's own Gram matrix
+  (stage-isolated weights and method variable) and simplex feasibility;
+* sampled buckets (first, last and two seeded others): the oracle's Gram,
+  its end-to-end weights and the update, as in the small-size tests;
+* 100k seeded element positions spread over all N: the update element
+  against the exactly computed weighted sum of the GPU weights (bf16 output:
+  the correctly rounded value; fp32 output: within K fp32 ulps of the sum
+  of magnitudes).
+"""
+
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from synth import WORKLOADS, fill_grads, host_rows
+from tests.parity import assert_gram, assert_out, assert_weights, run_resolve, singular_buckets
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+def _free():
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _check_workload(lib, wl, grads, offs, order):
+    print(f"case {wl.name}: K={wl.K} N={wl.N} B={wl.B} {wl.dtype} {wl.method}", flush=True)
+    res = run_resolve(lib, wl, grads, offs, order)
+    orders_np = wl.orders() if wl.method == "pcgrad" else None
+    # every bucket: stage-isolated solve and feasibility
+    w_iso, a_iso = oracle.solve(res["gram"], wl.method, wl.max_iter, wl.cagrad_c, orders_np)
+    assert_weights(res["weights"], w_iso, "weights(iso)", wl.name)
+    assert_weights(res["aux"], a_iso, "aux(iso)", wl.name)
+    assert np.all(np.isfinite(res["weights"]))
+    if wl.method in ("mgda", "cagrad"):
+        a = res["aux"]
+        assert a.min() >= -1e-12 and np.abs(a.sum(1) - 1).max() <= 1e-9
+    # sampled buckets end to end
+    offs_np = wl.offsets()
+    rng = np.random.default_rng(wl.seed)
+    picks = sorted({0, wl.B - 1, *rng.choice(wl.B, size=min(2, wl.B), replace=False).tolist()})
+    for b in picks:
+        lo, hi = int(offs_np[b]), int(offs_np[b + 1])
+        rows = host_rows(grads, lo, hi)
+        ob = np.array([0, hi - lo])
+        ora = oracle.resolve(rows, ob, wl.method, max_iter=wl.max_iter, cagrad_c=wl.cagrad_c,
+                             orders=None if orders_np is None else orders_np[b:b + 1])
+        assert_gram(res["gram"][b:b + 1], ora["gram"], wl.dtype, f"{wl.name} bucket {b}")
+        skip = singular_buckets(ora["gram"]) if wl.method in ("mgda", "cagrad") else None
+        assert_weights(res["weights"][b:b + 1], ora["weights"], "weights(e2e)", f"{wl.name} bucket {b}",
+                       skip=skip)
+        out_b = res["out"][lo:hi].cpu()
+        store = out_b.view(torch.int16).numpy().view(np.uint16) if out_b.dtype == torch.bfloat16 \
+            else out_b.numpy()
+        assert_out(store, oracle.decode_rows(rows), ob, res["weights"][b:b + 1], ora["weights"], wl.dtype,
+                   where=f"{wl.name} bucket {b}")
+        del rows, ora
+    # sampled elements over all of N
+    idx_np = np.sort(rng.choice(wl.N, size=100_000, replace=False)).astype(np.int64)
+    idx = torch.from_numpy(idx_np).to(grads.device)
+    xs = grads.index_select(1, idx)
+    xs_np = host_rows(xs, 0, xs.shape[1])
+    x64 = oracle.decode_rows(xs_np)
+    bucket = np.searchsorted(offs_np, idx_np, side="right") - 1
+    W = res["weights"][bucket]                              # [n, K]
+    exact = np.einsum("nk,kn->n", W, x64)
+    got_t = res["out"].index_select(0, idx).cpu()
+    if wl.dtype == "bf16":
+        got = got_t.view(torch.int16).numpy().view(np.uint16)
+        want = oracle.f64_to_bf16_bits(exact)
+        mism = np.mean(got != want)
+        assert mism <= 1e-4, f"{wl.name}: {mism:.2e} of sampled bf16 outputs not correctly rounded"
+    else:
+        got = got_t.numpy().astype(np.float64)
+        bound = wl.K * 2.0 ** -23 * np.einsum("nk,kn->n", np.abs(W), np.abs(x64)) + 1e-45
+        assert np.all(np.abs(got - exact) <= bound), f"{wl.name}: fp32 output off by more than K ulps"
+    del res, xs, got_t
+    print(f"  ok: buckets {picks} checked end to end", flush=True)
+
+
+@pytest.mark.parametrize("name", ["k2-mgda-1m-f32", "gpt2-124m-k4-pcgrad-f32", "llama3-8b-k4-mgda-bf16",
+                                  "llama3-8b-k8-cagrad-bf16"])
+def test_full_workload(gpu_lib, name):
+    _free()
+    wl = WORKLOADS[name]
+    grads = fill_grads(wl, device="cuda")
+    offs = torch.from_numpy(wl.offsets()).cuda()
+    order = torch.from_numpy(wl.orders()).cuda() if wl.method == "pcgrad" else None
+    try:
+        _check_workload(gpu_lib, wl, grads, offs, order)
+    finally:
+        del grads
+        _free()
+
+
+@pytest.mark.parametrize("mib", [1, 5, 25, 100])
+def test_full_qwen_k10_bucket_sweep(gpu_lib, mib):
+    """K=10 fp32 heavy-tailed gradients, one draw per bucket size, all three
+    methods on it."""
+    _free()
+    base = WORKLOADS[f"qwen-1.7b-k10-{mib}mib-mgda-f32"]
+    grads = fill_grads(base, device="cuda")
+    offs = torch.from_numpy(base.offsets()).cuda()
+    try:
+        for m in ("mgda", "pcgrad", "cagrad"):
+            wl = WORKLOADS[f"qwen-1.7b-k10-{mib}mib-{m}-f32"]
+            order = torch.from_numpy(wl.orders()).cuda() if m == "pcgrad" else None
+            _check_workload(gpu_lib, wl, grads, offs, order)
+    finally:
+        del grads
+        _free()
