@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run one plain elementwise kernel that reads 2 GiB and writes "
+                         "2 GiB (a known-size reference for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -128,6 +131,13 @@ def main():
             last[0] = time.time()
             log(f"  generated bucket {b + 1}/{B}")
 
+    if args.copy_calibration:
+        src = torch.ones(1 << 30, dtype=torch.bfloat16, device=dev)     # 2 GiB
+        flush = torch.zeros(1 << 31, dtype=torch.uint8, device=dev)     # evicts L2 and Infinity Cache
+        dst = torch.mul(src, 2.0)                                        # reads 2 GiB, writes 2 GiB
+        torch.cuda.synchronize()
+        log("copy calibration: elementwise kernel, 2 GiB read + 2 GiB written")
+        del src, dst, flush
     grads = fill_grads(wl, device=dev, progress=progress)
     torch.cuda.synchronize()
     log(f"generated in {time.time() - t0:.1f} s")
