@@ -4,10 +4,13 @@
 
 A step is one pass of the whole hot path over the workload's gradients,
 already resident in HBM: the per-bucket Gram matrices, the per-bucket solve
-and the combined update (the three stage entry points in stream order; the
-same kernels bkmoo_resolve launches, with identical results).  The default
-workload is the Llama-3-8B-shaped K=4 bf16 MGDA (Frank-Wolfe, 20 iterations)
-case with 25 MiB buckets.  Prints ONE JSON line.
+and the combined update.  The step runs what bkmoo_resolve runs for the
+workload: the single-read resident kernel when it applies (one call), else
+the two-pass kernels through the three stage entry points in stream order
+(identical results to bkmoo_resolve's two-pass path, and each stage can be
+timed).  The default workload is the Llama-3-8B-shaped K=4 bf16 MGDA
+(Frank-Wolfe, 20 iterations) case with 25 MiB buckets.  Prints ONE JSON
+line.
 
 Reported next to the throughput:
   roofline     the longest kernel of a step (HBM-bound), timed with HIP
@@ -102,6 +105,8 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--path", choices=["auto", "two-pass", "resident"], default="auto",
+                    help="force bkmoo_resolve's implementation (default: the library's choice)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run one plain elementwise kernel that reads 2 GiB and writes "
                          "2 GiB (a known-size reference for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
@@ -149,8 +154,21 @@ def main():
     W = torch.empty((B, K), dtype=torch.float32, device=dev)
     A = torch.empty((B, K), dtype=torch.float64, device=dev)
     stream = torch.cuda.current_stream(dev)
+    bkmoo.set_resolve_path({"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS,
+                            "resident": bkmoo.PATH_RESIDENT}[args.path])
+    path = bkmoo.resolve_path(grads, B + 1, wl.method, wl.max_iter)
+    resident = path == bkmoo.PATH_RESIDENT
+    log(f"resolve path: {'resident (single read)' if resident else 'two-pass'}")
 
     def step(ev=None):
+        if resident:
+            if ev is not None:
+                ev[0].record(stream)
+            bkmoo.resolve(grads, offs, wl.method, wl.max_iter, wl.cagrad_c, pcgrad_order=order, out=out,
+                          gram_out=G, weights=W, aux=A, workspace=ws)
+            if ev is not None:
+                ev[3].record(stream)
+            return
         if ev is not None:
             ev[0].record(stream)
         bkmoo.gram(grads, offs, gram_out=G, workspace=ws)
@@ -178,15 +196,21 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_start
     ms_step = t_wall * 1e3 / args.steps
-    st = {"gram": 0.0, "solve": 0.0, "combine": 0.0}
-    for ev in events:
-        st["gram"] += ev[0].elapsed_time(ev[1]) / args.steps
-        st["solve"] += ev[1].elapsed_time(ev[2]) / args.steps
-        st["combine"] += ev[2].elapsed_time(ev[3]) / args.steps
+    if resident:
+        st = {"resolve": sum(ev[0].elapsed_time(ev[3]) for ev in events) / args.steps}
+    else:
+        st = {"gram": 0.0, "solve": 0.0, "combine": 0.0}
+        for ev in events:
+            st["gram"] += ev[0].elapsed_time(ev[1]) / args.steps
+            st["solve"] += ev[1].elapsed_time(ev[2]) / args.steps
+            st["combine"] += ev[2].elapsed_time(ev[3]) / args.steps
     log(f"{ms_step:.3f} ms/step; stages (ms) " + ", ".join(f"{k} {v:.3f}" for k, v in st.items()))
 
-    # dominant kernel: the longer of the two streaming passes
-    if st["combine"] >= st["gram"]:
+    # dominant kernel: the resident kernel (reads K*s*N once, writes s*N), or
+    # the longer of the two streaming passes
+    if resident:
+        kname, kbytes, kms = "resident", (K + 1) * s * N, st["resolve"]
+    elif st["combine"] >= st["gram"]:
         kname, kbytes, kms = "combine", (K + 1) * s * N, st["combine"]
     else:
         kname, kbytes, kms = "gram", K * s * N, st["gram"]
@@ -210,6 +234,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "K": K, "N": N, "B": B, "bucket_elems": wl.bucket_elems,
                    "method": wl.method, "max_iter": wl.max_iter, "cagrad_c": wl.cagrad_c},
+        "path": "resident" if resident else "two-pass",
         "stages_ms": {k: round(v, 4) for k, v in st.items()},
         "resolve_algorithmic_GBps": round((2 * K + 1) * s * N / (ms_step / 1e3) / 1e9, 1),
         "roofline": roof,

@@ -81,7 +81,14 @@ typedef enum {
 } bkmoo_method;
 
 /* Device error word bits (bkmoo_read_device_error). */
-#define BKMOO_DEVERR_OFFSETS 0x1u
+#define BKMOO_DEVERR_OFFSETS 0x1u /* bucket offsets rejected */
+#define BKMOO_DEVERR_TIMEOUT 0x2u /* single-read resolve: a bounded wait expired (results invalid) */
+
+/* How bkmoo_resolve runs the step (bkmoo_resolve_path). */
+typedef enum {
+  BKMOO_PATH_TWO_PASS = 1, /* Gram pass, solve, combine pass: reads the gradients twice */
+  BKMOO_PATH_RESIDENT = 2  /* one cooperative kernel, each bucket held on chip: reads them once */
+} bkmoo_path;
 
 /* Hyper-parameters of the solve step (host struct). */
 typedef struct {
@@ -171,9 +178,24 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
 /*
  * bkmoo_resolve — gram, solve and combine in order on `stream` (one pass of
  * Algorithm 1's per-bucket loop over all buckets), with no host
- * synchronisation.  Results equal those of the three calls made one after
- * the other.  gram, weights and aux may be NULL, in which case the
+ * synchronisation.  gram, weights and aux may be NULL, in which case the
  * intermediate values live in the workspace only.
+ *
+ * Two implementations, same definitions and tolerances:
+ *   two-pass  the kernels of bkmoo_gram, bkmoo_solve and bkmoo_combine;
+ *             results equal those three calls bitwise.
+ *   resident  (K <= 4, 16-byte-phase-aligned rows and output) one
+ *             cooperative kernel keeps each bucket in registers and LDS
+ *             between its Gram and its combine, so every gradient element
+ *             is read from HBM once; the Gram sums run in a different (also
+ *             fixed, grid-independent) order, so results agree with the
+ *             two-pass path to rounding, not bitwise.  A bucket larger than
+ *             the chip holds is read twice, still correct.
+ * The resident path is chosen when the average bucket holds at least
+ * 32 MiB of gradients, fits on chip, and the solve is short (PCGrad, mean,
+ * or at most 2 Frank-Wolfe iterations): each bucket's solve lies on the
+ * resident kernel's critical path.  bkmoo_resolve_path reports the choice;
+ * bkmoo_set_resolve_path forces one.
  */
 bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
                            const int64_t *bucket_offsets, bkmoo_method method,
@@ -196,6 +218,31 @@ bkmoo_status bkmoo_read_device_error(const void *workspace, uint32_t *err, hipSt
  * independence.  Process-wide setting.
  */
 bkmoo_status bkmoo_set_grid_override(int32_t workgroups);
+
+/*
+ * bkmoo_resolve_path — the implementation bkmoo_resolve would use for these
+ * arguments on the current device (*path, host): BKMOO_PATH_TWO_PASS or
+ * BKMOO_PATH_RESIDENT.  `aligned` says whether every row and the output
+ * start at the same 16-byte phase.
+ */
+bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt, bkmoo_dtype out_dt,
+                                int32_t aligned, bkmoo_method method, int32_t max_iter,
+                                int32_t *path);
+
+/*
+ * bkmoo_set_resolve_path — force bkmoo_resolve's implementation
+ * (0: automatic, BKMOO_PATH_TWO_PASS, BKMOO_PATH_RESIDENT when eligible).
+ * Process-wide; for tests and tuning.
+ */
+bkmoo_status bkmoo_set_resolve_path(int32_t path);
+
+/*
+ * bkmoo_set_wait_limit — polls of the resident path's bounded wait for a
+ * bucket's weights before it gives up and sets BKMOO_DEVERR_TIMEOUT
+ * (default 4194304, about a second or more).  Process-wide; lets tests force
+ * the timeout path from the host.  0 is rejected.
+ */
+bkmoo_status bkmoo_set_wait_limit(uint32_t polls);
 
 /* Human-readable name of a status code (static string). */
 const char *bkmoo_status_string(bkmoo_status st);

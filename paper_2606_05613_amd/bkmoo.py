@@ -24,6 +24,8 @@ LIB_PATH = os.path.join(_HERE, "libbkmoo.so")
 F32, BF16 = 0, 1
 METHODS = {"mgda": 0, "pcgrad": 1, "cagrad": 2, "mean": 3}
 DEVERR_OFFSETS = 0x1
+DEVERR_TIMEOUT = 0x2
+PATH_TWO_PASS, PATH_RESIDENT = 1, 2
 
 
 class BkmooError(RuntimeError):
@@ -50,6 +52,10 @@ def _load():
                           vp, ctypes.c_int, vp, vp, vp, vp, sz, vp],
         "bkmoo_read_device_error": [vp, ctypes.POINTER(u32), vp],
         "bkmoo_set_grid_override": [i32],
+        "bkmoo_resolve_path": [i32, i64, i32, ctypes.c_int, ctypes.c_int, i32, ctypes.c_int, i32,
+                               ctypes.POINTER(i32)],
+        "bkmoo_set_resolve_path": [i32],
+        "bkmoo_set_wait_limit": [u32],
         "bkmoo_status_string": [ctypes.c_int],
     }
     for name, args in sig.items():
@@ -62,7 +68,8 @@ def _load():
 _lib = _load()
 
 EXPORTS = ("bkmoo_workspace_size", "bkmoo_gram", "bkmoo_solve", "bkmoo_combine", "bkmoo_resolve",
-           "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_status_string")
+           "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
+           "bkmoo_set_resolve_path", "bkmoo_set_wait_limit", "bkmoo_status_string")
 
 
 def status_string(st: int) -> str:
@@ -240,3 +247,26 @@ def read_device_error(workspace: torch.Tensor) -> int:
 
 def set_grid_override(workgroups: int):
     _check(_lib.bkmoo_set_grid_override(int(workgroups)), "bkmoo_set_grid_override")
+
+
+def resolve_path(grads: Grads, bucket_offsets_len: int, method: str = "mgda", max_iter: int = 20,
+                 out_dtype=None) -> int:
+    """PATH_TWO_PASS or PATH_RESIDENT: what resolve() would run for these
+    grads and method (output assumed aligned like the rows)."""
+    arr, dt, K, N, dev, rows = _rows(grads)
+    B = bucket_offsets_len - 1
+    odt = dt if out_dtype is None else _dt(torch.empty(0, dtype=out_dtype))
+    phases = {r.data_ptr() % 16 for r in rows}
+    out = ctypes.c_int32(0)
+    _check(_lib.bkmoo_resolve_path(K, N, B, dt, odt, int(len(phases) == 1), METHODS[method],
+                                   int(max_iter), ctypes.byref(out)), "bkmoo_resolve_path")
+    return out.value
+
+
+def set_resolve_path(path: int):
+    """0 automatic, PATH_TWO_PASS or PATH_RESIDENT (process-wide)."""
+    _check(_lib.bkmoo_set_resolve_path(int(path)), "bkmoo_set_resolve_path")
+
+
+def set_wait_limit(polls: int):
+    _check(_lib.bkmoo_set_wait_limit(int(polls)), "bkmoo_set_wait_limit")

@@ -6,12 +6,20 @@ Every translation unit under csrc/ is compiled in parallel into _build/ and
 linked into paper_2606_05613_amd/libbkmoo.so.  All device code is built with
 packed-fp32 instruction selection disabled; the solver additionally without
 floating-point contraction so its scalar expressions round as written.
+
+After compiling, the generated gfx950 assembly is checked for a vector-memory
+store of more than 64 bits whose data registers an immediately following
+vector instruction overwrites: the store reads its data over two cycles and
+such an overwrite corrupts the stored value.  The build fails if the pattern
+appears.
 """
 
 from __future__ import annotations
 
 import concurrent.futures
+import glob
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -24,8 +32,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbkmoo.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "schedule.hip", "gram.hip", "solve.hip", "combine.hip"]
-EXTRA = {"solve.hip": ["-ffp-contract=off"]}
+SOURCES = ["api.hip", "schedule.hip", "gram.hip", "solve.hip", "combine.hip", "resident.hip"]
+EXTRA = {"solve.hip": ["-ffp-contract=off"], "resident.hip": ["-ffp-contract=off"]}
 
 
 def hipcc() -> str:
@@ -43,17 +51,53 @@ def common_flags():
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-    cmd = [hipcc()] + common_flags() + EXTRA.get(src, []) + ["-c", os.path.join(CSRC, src), "-o", obj]
-    r = subprocess.run(cmd, capture_output=True, text=True)
+    cmd = [hipcc()] + common_flags() + EXTRA.get(src, []) + ["-save-temps=obj", "-c",
+                                                             os.path.join(CSRC, src), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True, cwd=BUILD)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr[-6000:]}")
     return obj
+
+
+def _vgprs(op: str):
+    m = re.match(r"v\[(\d+):(\d+)\]", op)
+    if m:
+        return set(range(int(m.group(1)), int(m.group(2)) + 1))
+    m = re.match(r"v(\d+)$", op)
+    return {int(m.group(1))} if m else set()
+
+
+def store_data_overwrites(asm_path: str):
+    """(line, store, next instruction) where a >64-bit vector store is
+    followed directly by a vector instruction writing its data registers."""
+    lines = [ln.split(";")[0].strip() for ln in open(asm_path)]
+    found = []
+    for i, ln in enumerate(lines):
+        m = re.match(r"(buffer|global|flat|scratch)_store_(dwordx3|dwordx4|b96|b128)\s+(.*)", ln)
+        if not m:
+            continue
+        ops = [o.strip() for o in m.group(3).split(",")]
+        data = _vgprs(ops[0] if m.group(1) == "buffer" else ops[1])
+        for nxt in lines[i + 1:i + 4]:
+            if not nxt or nxt.startswith("."):
+                continue
+            w = re.match(r"v_\w+\s+([^,]+)", nxt)
+            if w and _vgprs(w.group(1).strip()) & data:
+                found.append((i + 1, ln, nxt))
+            break
+    return found
 
 
 def build(jobs: int = 8) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with concurrent.futures.ThreadPoolExecutor(max_workers=jobs) as ex:
         objs = list(ex.map(_compile, SOURCES))
+    bad = []
+    for asm in glob.glob(os.path.join(BUILD, f"*-hip-amdgcn-amd-amdhsa-{ARCH}.s")):
+        bad += [(os.path.basename(asm),) + h for h in store_data_overwrites(asm)]
+    if bad:
+        detail = "\n".join(f"{a}:{ln}: {st}  ->  {nx}" for a, ln, st, nx in bad[:20])
+        raise RuntimeError(f"{len(bad)} store-data overwrite hazards in the generated code:\n{detail}")
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -12,6 +12,17 @@ namespace bkmoo {
 namespace {
 
 std::atomic<int> g_grid_override{0};
+std::atomic<int> g_resolve_path{0};            // 0 automatic, 1 two-pass, 2 resident
+std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the resident path's bounded wait
+
+// Resident single-read resolve pays when a bucket is large enough to
+// amortise its grid-wide barrier, small enough to stay on chip, and its
+// solve is short: the solve of each bucket sits on the kernel's critical
+// path (a 20-iteration Frank-Wolfe costs about 7 us per bucket there, more
+// than the second read it saves on 25 MiB buckets), so iterative solvers
+// stay on the two-pass path unless they run at most kResidentMaxIters.
+constexpr double kResidentMinBucketBytes = 32.0 * (1 << 20);
+constexpr int kResidentMaxIters = 2;
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cu_count[kMaxDevices];
@@ -81,6 +92,7 @@ struct Carved {
   double *gram;
   float *weights;
   double *partials;
+  uint32_t *sync;
 };
 
 Carved carve(void *ws, const Layout &L) {
@@ -88,7 +100,26 @@ Carved carve(void *ws, const Layout &L) {
   return Carved{reinterpret_cast<uint32_t *>(base + L.err),
                 reinterpret_cast<int64_t *>(base + L.chunk_start),
                 reinterpret_cast<double *>(base + L.gram), reinterpret_cast<float *>(base + L.weights),
-                reinterpret_cast<double *>(base + L.partials)};
+                reinterpret_cast<double *>(base + L.partials), reinterpret_cast<uint32_t *>(base + L.sync)};
+}
+
+// Workgroups for the resident path, or 0 when it should not be used.
+int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters) {
+  const int mode = g_resolve_path.load();
+  if (mode == 1 || K > 4 || !vec) return 0;
+  static std::atomic<int> cache[3][2][2];  // K-2, dt, out_dt (device model is fixed per process here)
+  int g = cache[K - 2][dt][out_dt].load();
+  if (g == 0) {
+    g = resident_grid(K, dt, out_dt);
+    cache[K - 2][dt][out_dt].store(g > 0 ? g : -1);
+  }
+  if (g <= 0) return 0;
+  if (mode == 2) return g;
+  const double avg_elems = (double)N / B;
+  const double bucket_bytes = avg_elems * K * elem_bytes(dt);
+  const double fits = (double)resident_segment_elems(K, dt) * g;
+  const bool cheap_solve = method == BKMOO_PCGRAD || method == BKMOO_MEAN || iters <= kResidentMaxIters;
+  return bucket_bytes >= kResidentMinBucketBytes && avg_elems <= fits && cheap_solve ? g : 0;
 }
 
 }  // namespace
@@ -133,7 +164,8 @@ bkmoo_status bkmoo_gram(int32_t K, const void *const *grads, bkmoo_dtype dt, int
   const Layout L = layout(K, N, B, dt);
   if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
   const Carved w = carve(workspace, L);
-  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err, stream);
+  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err,
+                                 nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
   const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec,
                      g_grid_override.load()};
@@ -166,7 +198,8 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   const Layout L = layout(K, N, B, dt);
   if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
   const Carved w = carve(workspace, L);
-  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err, stream);
+  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err,
+                                 nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
   const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec,
                      g_grid_override.load()};
@@ -192,15 +225,27 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   const Carved w = carve(workspace, L);
   double *G = gram ? gram : w.gram;
   float *W = weights ? weights : w.weights;
+  const int iters = hp ? hp->max_iter : 0;
+  const double c = hp ? hp->cagrad_c : 0.0;
+  const int8_t *order = hp ? hp->pcgrad_order : nullptr;
 
-  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err, stream);
+  const int rgrid = choose_resident(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters);
+  if (rgrid > 0) {
+    hipError_t e = launch_schedule(bucket_offsets, B, N, resident_segment_elems(K, dt), w.chunk_start,
+                                   w.err, w.sync, 2 * (int64_t)B, stream);
+    if (e != hipSuccess) return BKMOO_EHIP;
+    e = launch_resident(K, (int)dt, (int)out_dt, grads, bucket_offsets, w.chunk_start, B, shift,
+                        (int)method, iters, c, order, G, W, aux, out, w.partials, w.sync, w.sync + B,
+                        w.err, g_spin_limit.load(), rgrid, stream);
+    return hip_status(e);
+  }
+
+  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err,
+                                 nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
   StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec_in,
                g_grid_override.load()};
   if ((e = launch_gram(a, w.partials, G, stream)) != hipSuccess) return BKMOO_EHIP;
-  const int iters = hp ? hp->max_iter : 0;
-  const double c = hp ? hp->cagrad_c : 0.0;
-  const int8_t *order = hp ? hp->pcgrad_order : nullptr;
   if ((e = launch_solve(K, B, G, (int)method, iters, c, order, W, aux, stream)) != hipSuccess)
     return BKMOO_EHIP;
   a.vec = vec_out;
@@ -220,6 +265,31 @@ bkmoo_status bkmoo_read_device_error(const void *workspace, uint32_t *err, hipSt
 bkmoo_status bkmoo_set_grid_override(int32_t workgroups) {
   if (workgroups < 0) return BKMOO_EINVAL;
   g_grid_override.store(workgroups);
+  return BKMOO_OK;
+}
+
+bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt, bkmoo_dtype out_dt,
+                                int32_t aligned, bkmoo_method method, int32_t max_iter,
+                                int32_t *path) {
+  if (!path) return BKMOO_EINVAL;
+  const bkmoo_status st = check_shape(K, N, B, dt);
+  if (st != BKMOO_OK) return st;
+  if (!valid_dtype(out_dt) || method < BKMOO_MGDA || method > BKMOO_MEAN) return BKMOO_EINVAL;
+  *path = choose_resident(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter) > 0
+              ? BKMOO_PATH_RESIDENT
+              : BKMOO_PATH_TWO_PASS;
+  return BKMOO_OK;
+}
+
+bkmoo_status bkmoo_set_resolve_path(int32_t path) {
+  if (path < 0 || path > 2) return BKMOO_EINVAL;
+  g_resolve_path.store(path);
+  return BKMOO_OK;
+}
+
+bkmoo_status bkmoo_set_wait_limit(uint32_t polls) {
+  if (polls == 0) return BKMOO_EINVAL;
+  g_spin_limit.store(polls);
   return BKMOO_OK;
 }
 

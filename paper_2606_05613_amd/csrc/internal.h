@@ -40,8 +40,9 @@ constexpr int pairs(int K) { return K * (K + 1) / 2; }
 //   gram                fp64  [B][K][K]   (used when the caller passes none)
 //   weights             fp32  [B][K]      (used when the caller passes none)
 //   partials            fp64  [cap][P]    cap = ceil(N / C) + B
+//   sync                uint32 [2][B]     resident path: arrival counters, flags
 struct Layout {
-  size_t err, chunk_start, gram, weights, partials, total;
+  size_t err, chunk_start, gram, weights, partials, sync, total;
   int64_t cap_chunks;
 };
 
@@ -57,11 +58,13 @@ inline Layout layout(int K, int64_t N, int B, int dt) {
   L.gram = o;           o = align256(o + sizeof(double) * (size_t)B * K * K);
   L.weights = o;        o = align256(o + sizeof(float) * (size_t)B * K);
   L.partials = o;       o = align256(o + sizeof(double) * (size_t)L.cap_chunks * pairs(K));
+  L.sync = o;           o = align256(o + sizeof(uint32_t) * 2 * (size_t)B);
   L.total = o;
   return L;
 }
 
 constexpr uint32_t kErrOffsets = 0x1u;
+constexpr uint32_t kErrTimeout = 0x2u;
 
 // Pointers of the K task rows, passed by value as kernel arguments.
 template <int K>
@@ -85,13 +88,25 @@ struct StreamArgs {
   int grid;                    // workgroups (0: automatic)
 };
 
+// Validates offsets, writes chunk_start for chunks of C elements, clears the
+// error word and zeroes `nsync` words at `sync` (may be null).
 hipError_t launch_schedule(const int64_t *offsets, int B, int64_t N, int64_t C, int64_t *chunk_start,
-                           uint32_t *err, hipStream_t s);
+                           uint32_t *err, uint32_t *sync, int64_t nsync, hipStream_t s);
 hipError_t launch_gram(const StreamArgs &a, double *partials, double *gram, hipStream_t s);
 hipError_t launch_solve(int K, int B, const double *gram, int method, int max_iter, double c,
                         const int8_t *order, float *weights, double *aux, hipStream_t s);
 hipError_t launch_combine(const StreamArgs &a, const float *weights, void *out, int out_dt,
                           hipStream_t s);
+
+// Single-read resident resolve (K <= 4): elements per segment, workgroups
+// of the cooperative launch (0 if the combination cannot run resident).
+int64_t resident_segment_elems(int K, int dt);
+int resident_grid(int K, int dt, int out_dt);
+hipError_t launch_resident(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs,
+                           const int64_t *seg_start, int B, int shift, int method, int iters, double c,
+                           const int8_t *order, double *gram, float *weights, double *aux, void *out,
+                           double *partials, uint32_t *arrive, uint32_t *flags, uint32_t *err,
+                           uint32_t spin_limit, int grid, hipStream_t s);
 
 int device_cu_count();
 

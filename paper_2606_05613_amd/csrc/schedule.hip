@@ -14,11 +14,12 @@ constexpr int kSchedThreads = 1024;
 // gets kErrOffsets.  Otherwise the error word is cleared.
 __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
     const int64_t *__restrict__ offs, int B, int64_t N, int64_t C, int64_t *__restrict__ cs,
-    uint32_t *__restrict__ err) {
+    uint32_t *__restrict__ err, uint32_t *__restrict__ sync, int64_t nsync) {
   __shared__ int bad;
   __shared__ int64_t scan[kSchedThreads];
   __shared__ int64_t carry;
   const int tid = threadIdx.x;
+  for (int64_t i = tid; i < nsync; i += kSchedThreads) sync[i] = 0u;
   if (tid == 0) {
     bad = (offs[0] != 0 || offs[B] != N) ? 1 : 0;
     carry = 0;
@@ -59,9 +60,9 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(
 }  // namespace
 
 hipError_t launch_schedule(const int64_t *offsets, int B, int64_t N, int64_t C, int64_t *chunk_start,
-                           uint32_t *err, hipStream_t s) {
+                           uint32_t *err, uint32_t *sync, int64_t nsync, hipStream_t s) {
   hipLaunchKernelGGL(schedule_kernel, dim3(1), dim3(kSchedThreads), 0, s, offsets, B, N, C,
-                     chunk_start, err);
+                     chunk_start, err, sync, nsync);
   return hipGetLastError();
 }
 

@@ -44,6 +44,28 @@ __device__ __forceinline__ u32x4 stream_load(const void *base, int64_t vec_index
   return __builtin_nontemporal_load(static_cast<const u32x4 *>(base) + vec_index);
 }
 
+// Raw buffer access: address = descriptor base (scalar) + per-lane byte
+// offset + scalar byte offset, range-checked against the descriptor's size
+// (loads beyond it return 0, stores beyond it are dropped).  Keeps address
+// arithmetic out of vector registers when a thread touches many vectors.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr int kRawBufferDword3 = 0x00020000;  // untyped buffer view on gfx9-family parts
+constexpr int kNonTemporal = 2;               // cache policy: streaming (nt)
+
+__device__ __forceinline__ Rsrc make_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                           kRawBufferDword3);
+}
+__device__ __forceinline__ u32x4 buf_load16(Rsrc r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, kNonTemporal);
+}
+__device__ __forceinline__ void buf_store16(u32x4 v, Rsrc r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (int)voff, (int)soff, kNonTemporal);
+}
+__device__ __forceinline__ void buf_store8(u32x2 v, Rsrc r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, (int)voff, (int)soff, kNonTemporal);
+}
+
 // Bucket of chunk c: the b with chunk_start[b] <= c < chunk_start[b+1].
 // chunk_start is non-decreasing (empty buckets repeat a value).
 __device__ __forceinline__ int find_bucket(const int64_t *__restrict__ cs, int B, int64_t c) {

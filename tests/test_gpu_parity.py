@@ -70,6 +70,8 @@ def test_output_dtype_conversion(gpu_lib, dtype, out_dtype):
 
 
 def test_stage_calls_equal_resolve_bitwise(gpu_lib):
+    """The two-pass resolve is exactly the three stage calls."""
+    gpu_lib.set_resolve_path(gpu_lib.PATH_TWO_PASS)
     wl = small_workload(BASE["cagrad"], sum(LENS), bucket_lens=LENS, seed=99)
     grads, offs, order = to_device_inputs(wl)
     res = run_resolve(gpu_lib, wl, grads, offs, order)
@@ -77,6 +79,7 @@ def test_stage_calls_equal_resolve_bitwise(gpu_lib):
     W, A = gpu_lib.solve(G, wl.method, wl.max_iter, wl.cagrad_c)
     out = gpu_lib.combine(grads, offs, W)
     torch.cuda.synchronize()
+    gpu_lib.set_resolve_path(0)
     assert np.array_equal(G.cpu().numpy(), res["gram"])
     assert np.array_equal(W.cpu().numpy().astype(np.float64), res["weights"])
     assert np.array_equal(A.cpu().numpy(), res["aux"])
