@@ -164,7 +164,7 @@ bkmoo_status bkmoo_gram(int32_t K, const void *const *grads, bkmoo_dtype dt, int
   const Layout L = layout(K, N, B, dt);
   if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
   const Carved w = carve(workspace, L);
-  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err,
+  hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start, w.err,
                                  nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
   const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec,
@@ -198,8 +198,8 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   const Layout L = layout(K, N, B, dt);
   if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
   const Carved w = carve(workspace, L);
-  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err,
-                                 nullptr, 0, stream);
+  hipError_t e = launch_schedule(bucket_offsets, B, N, combine_chunk_elems(K, dt), w.chunk_start,
+                                 w.err, nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
   const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec,
                      g_grid_override.load()};
@@ -240,7 +240,7 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
     return hip_status(e);
   }
 
-  hipError_t e = launch_schedule(bucket_offsets, B, N, chunk_elems(K, dt), w.chunk_start, w.err,
+  hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start, w.err,
                                  nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
   StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec_in,
@@ -248,6 +248,11 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   if ((e = launch_gram(a, w.partials, G, stream)) != hipSuccess) return BKMOO_EHIP;
   if ((e = launch_solve(K, B, G, (int)method, iters, c, order, W, aux, stream)) != hipSuccess)
     return BKMOO_EHIP;
+  // the combine pass cuts its own chunks (the schedule keeps the error word
+  // the Gram pass's schedule set: offsets are the same)
+  e = launch_schedule(bucket_offsets, B, N, combine_chunk_elems(K, dt), w.chunk_start, w.err, nullptr,
+                      0, stream);
+  if (e != hipSuccess) return BKMOO_EHIP;
   a.vec = vec_out;
   return hip_status(launch_combine(a, W, out, (int)out_dt, stream));
 }

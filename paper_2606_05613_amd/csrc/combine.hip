@@ -26,9 +26,9 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(
     Rows<K> rows, const int64_t *__restrict__ offs, const int64_t *__restrict__ cs, int B,
     int shift, int vec, const float *__restrict__ weights, void *out) {
   constexpr int V = vec_elems(DT);
-  constexpr int R = rows_per_thread(K);
-  constexpr int U = iters_per_chunk(K);
-  constexpr int64_t C = chunk_elems(K, DT);
+  constexpr int R = combine_shape(K).R;
+  constexpr int U = combine_shape(K).U;
+  constexpr int64_t C = combine_chunk_elems(K, DT);
   constexpr int EB = elem_bytes(DT);
 
   int64_t c, cend;
@@ -102,7 +102,7 @@ hipError_t launch_combine_t(const StreamArgs &a, const float *weights, void *out
   Rows<K> rows;
   for (int i = 0; i < K; ++i) rows.p[i] = a.rows[i];
   auto kern = combine_kernel<K, DT, ODT>;
-  const int64_t C = chunk_elems(K, DT);
+  const int64_t C = combine_chunk_elems(K, DT);
   const int64_t cap = (a.N + C - 1) / C + a.B;
   static const int occ = occupancy(kern);
   int64_t grid = a.grid > 0 ? a.grid : (int64_t)device_cu_count() * occ;

@@ -38,9 +38,9 @@ __global__ __launch_bounds__(kThreads) void gram_partial_kernel(
     Rows<K> rows, const int64_t *__restrict__ offs, const int64_t *__restrict__ cs, int B,
     int shift, int vec, double *__restrict__ partials) {
   constexpr int V = vec_elems(DT);
-  constexpr int R = rows_per_thread(K);
-  constexpr int U = iters_per_chunk(K);
-  constexpr int64_t C = chunk_elems(K, DT);
+  constexpr int R = gram_shape(K).R;
+  constexpr int U = gram_shape(K).U;
+  constexpr int64_t C = gram_chunk_elems(K, DT);
   constexpr int P = pairs(K);
   constexpr int EB = elem_bytes(DT);
   __shared__ double red[kThreads / kWave][P];
@@ -160,7 +160,7 @@ hipError_t launch_gram_t(const StreamArgs &a, double *partials, hipStream_t s) {
   Rows<K> rows;
   for (int i = 0; i < K; ++i) rows.p[i] = a.rows[i];
   auto kern = gram_partial_kernel<K, DT>;
-  const int64_t C = chunk_elems(K, DT);
+  const int64_t C = gram_chunk_elems(K, DT);
   const int64_t cap = (a.N + C - 1) / C + a.B;
   static const int occ = occupancy(kern);
   int64_t grid = a.grid > 0 ? a.grid : (int64_t)device_cu_count() * occ;

@@ -18,19 +18,25 @@ enum Dtype : int { F32 = 0, BF16 = 1 };
 constexpr int vec_elems(int dt) { return dt == F32 ? 4 : 8; }
 constexpr int elem_bytes(int dt) { return dt == F32 ? 4 : 2; }
 
-// 16-byte vectors each thread loads per task row and iteration, and
-// iterations per chunk.  K * R bounds the registers holding loaded data
-// (4 per vector) next to K(K+1)/2 fp32 accumulators; occupancy (several
-// wavefronts per SIMD) supplies the rest of the memory-level parallelism.
-constexpr int rows_per_thread(int K) { return K <= 8 ? 2 : 1; }
-constexpr int iters_per_chunk(int K) { return K <= 8 ? 8 : 16; }
+// Streaming-pass shapes.  A chunk is U iterations of kThreads * R 16-byte
+// vectors per task row; chunks never straddle buckets, so bucket b holds
+// ceil(n_b / C) chunks.  K * R bounds the registers holding loaded data (4
+// per vector) next to the pass's accumulators; occupancy supplies the rest
+// of the memory-level parallelism.  The two passes are tuned separately
+// (measured on MI355X): the Gram pass prefers long chunks (fewer fixed-order
+// reductions), the combine pass shorter ones.  Each thread accumulates
+// R * U * V elements of a chunk in fp32 in the Gram pass.
+struct PassShape {
+  int R, U;
+};
+constexpr PassShape gram_shape(int K) { return K <= 8 ? PassShape{2, 8} : PassShape{1, 16}; }
+constexpr PassShape combine_shape(int K) { return K <= 8 ? PassShape{2, 4} : PassShape{1, 8}; }
 
-// A chunk is the unit of streaming work: U iterations of kThreads * R
-// vectors.  Chunks never straddle buckets, so bucket b holds ceil(n_b / C)
-// chunks.  Each thread accumulates R * U * V elements of a chunk in fp32.
-constexpr int64_t chunk_elems(int K, int dt) {
-  return (int64_t)kThreads * rows_per_thread(K) * iters_per_chunk(K) * vec_elems(dt);
+constexpr int64_t shape_elems(PassShape p, int dt) {
+  return (int64_t)kThreads * p.R * p.U * vec_elems(dt);
 }
+constexpr int64_t gram_chunk_elems(int K, int dt) { return shape_elems(gram_shape(K), dt); }
+constexpr int64_t combine_chunk_elems(int K, int dt) { return shape_elems(combine_shape(K), dt); }
 
 constexpr int pairs(int K) { return K * (K + 1) / 2; }
 
@@ -50,7 +56,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 inline Layout layout(int K, int64_t N, int B, int dt) {
   Layout L;
-  const int64_t C = chunk_elems(K, dt);
+  const int64_t C = gram_chunk_elems(K, dt);  // the smallest chunk with partial slots
   L.cap_chunks = (N + C - 1) / C + B;
   size_t o = 0;
   L.err = o;            o += 256;
