@@ -18,6 +18,8 @@ Parity status of each function (what pins it is listed in its docstring):
   tiny buckets, no-conflict and K=2 closed forms)
 * cagrad_fw / cagrad_exact ............ pinned (primal feasibility, zero
   duality gap, random-direction search, c=0 reduction, descent bound)
+* conflicts ........................... pinned (cosines and conflict counts
+  from the vectors, closed-form configurations, invariances)
 """
 
 from .reference import (  # noqa: F401
@@ -25,6 +27,7 @@ from .reference import (  # noqa: F401
     cagrad_exact,
     cagrad_fw,
     combine,
+    conflicts,
     decode_rows,
     f64_to_bf16_bits,
     gram,

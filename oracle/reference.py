@@ -354,6 +354,70 @@ def cagrad_exact(G: np.ndarray, c: float):
 
 
 # ----------------------------------------------------------------------------
+# Conflict diagnostics (the conflicting-gradients definition of Section 2.1
+# and its appendix restatement; the statistics of Figure 1)
+# ----------------------------------------------------------------------------
+
+
+def conflicts(grams: np.ndarray):
+    """Per-bucket gradient-conflict statistics from the Gram matrices.
+
+    Two task gradients conflict when their inner product is negative
+    (equivalently, their cosine similarity is negative).  Figure 1 tracks the
+    mean and standard deviation of the pairwise cosine similarities over all
+    task pairs, and counts a conflict at a step when at least one pair has a
+    negative cosine.  Per bucket b, over the pairs i < j in lexicographic
+    order:
+
+      cos[b, i, j] = G_ij / sqrt(G_ii G_jj), clipped to [-1, 1]; 0 when either
+                     gradient is zero (no direction, so no conflict); the
+                     diagonal is 1 for a nonzero gradient and 0 otherwise
+      summary[b]   = (mean, population standard deviation, minimum) of the
+                     K(K-1)/2 pairwise cosines
+      pairs[b]     = (i, j) of the smallest cosine (first pair on ties) and the
+                     number of pairs with G_ij < 0; a count > 0 is Figure 1's
+                     per-step conflict event
+
+    A bucket whose Gram holds a NaN or infinity gets NaN cosines and summary
+    and pairs (-1, -1, -1).  Returns (cos [B, K, K], summary [B, 3] float64,
+    pairs [B, 3] int64).
+    """
+    grams = np.asarray(grams, dtype=np.float64)
+    nb, k, _ = grams.shape
+    cos = np.zeros((nb, k, k))
+    summary = np.empty((nb, 3))
+    pairs = np.empty((nb, 3), dtype=np.int64)
+    for b in range(nb):
+        G = grams[b]
+        if not np.all(np.isfinite(G)):
+            cos[b] = np.nan
+            summary[b] = np.nan
+            pairs[b] = -1
+            continue
+        vals = []
+        count = 0
+        best = None
+        for i in range(k):
+            cos[b, i, i] = 1.0 if G[i, i] > 0.0 else 0.0
+            for j in range(i + 1, k):
+                if G[i, i] > 0.0 and G[j, j] > 0.0:
+                    c = G[i, j] / math.sqrt(G[i, i] * G[j, j])
+                    c = min(max(c, -1.0), 1.0)
+                else:
+                    c = 0.0
+                cos[b, i, j] = cos[b, j, i] = c
+                vals.append(c)
+                if G[i, j] < 0.0:
+                    count += 1
+                if best is None or c < best[0]:
+                    best = (c, i, j)
+        v = np.array(vals)
+        summary[b] = (v.mean(), v.std(), best[0])
+        pairs[b] = (best[1], best[2], count)
+    return cos, summary, pairs
+
+
+# ----------------------------------------------------------------------------
 # per-bucket solve, combine and the whole resolve step (Algorithm 1)
 # ----------------------------------------------------------------------------
 

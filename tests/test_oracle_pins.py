@@ -435,6 +435,100 @@ def test_resolve_is_bucketwise_concatenation():
 
 
 # ----------------------------------------------------------------------------
+# conflict diagnostics: cosines and counts from the vectors themselves
+# ----------------------------------------------------------------------------
+
+
+def _vector_conflicts(x, offs):
+    """Cosines, (mean, population std, min), (argmin pair, count) computed
+    from the gradient vectors with numpy norms and statistics routines."""
+    import statistics
+    k = x.shape[0]
+    res = []
+    for b in range(len(offs) - 1):
+        xb = x[:, offs[b]:offs[b + 1]]
+        cos, neg = {}, 0
+        for i, j in itertools.combinations(range(k), 2):
+            ni, nj = np.linalg.norm(xb[i]), np.linalg.norm(xb[j])
+            d = math.fsum(xb[i] * xb[j])
+            cos[(i, j)] = 0.0 if ni == 0 or nj == 0 else max(-1.0, min(1.0, d / (ni * nj)))
+            neg += d < 0
+        vals = list(cos.values())
+        m = min(vals)
+        first = next(pq for pq in itertools.combinations(range(k), 2) if cos[pq] == m)
+        res.append((cos, statistics.fmean(vals), statistics.pstdev(vals), m, first, neg))
+    return res
+
+
+def check_conflicts(fn):
+    rng = np.random.default_rng(21)
+    lens = [40, 1, 17, 64]
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    x = rand_grads(rng, 5, offs[-1], corr=rand_corr(rng, 5, -0.7, 0.7))
+    x[3, offs[2]:offs[3]] = 0.0                 # a zero gradient in bucket 2
+    grams = np.stack([x[:, offs[b]:offs[b + 1]] @ x[:, offs[b]:offs[b + 1]].T for b in range(4)])
+    cos, summ, pairs = fn(grams)
+    for b, (vc, mean, std, m, first, neg) in enumerate(_vector_conflicts(x, offs)):
+        for (i, j), c in vc.items():
+            assert abs(cos[b, i, j] - c) <= 1e-12 and abs(cos[b, j, i] - c) <= 1e-12
+        norms = np.linalg.norm(x[:, offs[b]:offs[b + 1]], axis=1)
+        assert np.array_equal(np.diag(cos[b]), (norms > 0).astype(float))
+        assert abs(summ[b, 0] - mean) <= 1e-12 and abs(summ[b, 1] - std) <= 1e-12
+        assert abs(summ[b, 2] - m) <= 1e-12
+        assert tuple(pairs[b, :2]) == first and pairs[b, 2] == neg
+    # exact ties (orthogonal unit vectors): the first pair wins, none conflicts
+    e = np.eye(4)[:3]
+    cos, summ, pairs = fn((e @ e.T)[None])
+    assert tuple(pairs[0]) == (0, 1, 0) and summ[0, 0] == 0.0 and summ[0, 1] == 0.0
+
+
+def test_conflicts_match_vector_cosines():
+    check_conflicts(oracle.conflicts)
+
+
+def test_conflicts_closed_forms():
+    # e1, e2, e1+e2: cosines 0, 1/sqrt2, 1/sqrt2 -> mean sqrt2/3, std 1/3
+    x = np.array([[1.0, 0.0], [0.0, 1.0], [1.0, 1.0]])
+    _, summ, pairs = oracle.conflicts((x @ x.T)[None])
+    assert abs(summ[0, 0] - math.sqrt(2) / 3) <= 1e-15 and abs(summ[0, 1] - 1 / 3) <= 1e-15
+    assert summ[0, 2] == 0.0 and tuple(pairs[0]) == (0, 1, 0)
+    # three unit vectors 120 degrees apart: every pair conflicts at cos -1/2
+    ang = np.array([0.0, 2 * np.pi / 3, 4 * np.pi / 3])
+    x = np.stack([np.cos(ang), np.sin(ang)], 1)
+    _, summ, pairs = oracle.conflicts((x @ x.T)[None])
+    assert abs(summ[0, 0] + 0.5) <= 1e-15 and summ[0, 1] <= 1e-15 and pairs[0, 2] == 3
+    # opposite and parallel pairs
+    x = np.array([[1.0, 2.0, -3.0], [-2.0, -4.0, 6.0], [0.5, 1.0, -1.5]])
+    cos, summ, pairs = oracle.conflicts((x @ x.T)[None])
+    assert cos[0, 0, 1] == -1.0 and cos[0, 0, 2] == 1.0 and pairs[0, 2] == 2
+    assert tuple(pairs[0, :2]) == (0, 1)
+
+
+def test_conflicts_invariances():
+    rng = np.random.default_rng(22)
+    x = rand_grads(rng, 4, 50, corr=rand_corr(rng, 4, -0.8, 0.8))
+    cos, _, pairs = oracle.conflicts((x @ x.T)[None])
+    s = np.array([3.0, 0.25, 7.0, 1.5])          # positive per-task scales
+    xs = x * s[:, None]
+    cos_s, _, pairs_s = oracle.conflicts((xs @ xs.T)[None])
+    np.testing.assert_allclose(cos_s, cos, atol=1e-14)
+    assert pairs_s[0, 2] == pairs[0, 2]
+    xf = x.copy()
+    xf[1] *= -1.0                                 # negating a task flips its row
+    cos_f, _, _ = oracle.conflicts((xf @ xf.T)[None])
+    sign = np.ones(4)
+    sign[1] = -1.0
+    np.testing.assert_allclose(cos_f[0], cos[0] * np.outer(sign, sign), atol=1e-14)
+
+
+def test_conflicts_non_finite_bucket():
+    G = np.stack([np.eye(3), np.full((3, 3), np.nan)])
+    cos, summ, pairs = oracle.conflicts(G)
+    assert np.all(np.isnan(cos[1])) and np.all(np.isnan(summ[1])) and np.all(pairs[1] == -1)
+    assert tuple(pairs[0]) == (0, 1, 0)
+
+
+# ----------------------------------------------------------------------------
 # the pins catch plausible mistakes planted in the oracle (on the CPU)
 # ----------------------------------------------------------------------------
 
@@ -501,6 +595,7 @@ def test_checks_pass_on_the_oracle():
     check_pcgrad(oracle.pcgrad)
     check_cagrad(oracle.cagrad_exact)
     check_combine(oracle.combine)
+    check_conflicts(oracle.conflicts)
 
 
 def _gram_off_by_one(x, offs):
@@ -563,6 +658,35 @@ def _combine_first_bucket_weights(x, offs, W):
     return out
 
 
+def _conflicts_mutant(**change):
+    """The oracle's conflicts() with one plausible mistake planted."""
+    def fn(grams):
+        grams = np.asarray(grams, dtype=np.float64)
+        nb, k, _ = grams.shape
+        cos = np.zeros((nb, k, k))
+        summ = np.empty((nb, 3))
+        pairs = np.empty((nb, 3), dtype=np.int64)
+        for b in range(nb):
+            G = grams[b]
+            vals, count, best = [], 0, None
+            for i in range(k):
+                cos[b, i, i] = 1.0 if G[i, i] > 0 else 0.0
+                for j in range(i + 1, k):
+                    den = G[i, i] * G[j, j] if change.get("no_sqrt") else math.sqrt(G[i, i] * G[j, j])
+                    c = 0.0 if den == 0 else max(-1.0, min(1.0, G[i, j] / den))
+                    cos[b, i, j] = cos[b, j, i] = c
+                    vals.append(c)
+                    count += (G[i, j] <= 0) if change.get("le") else (G[i, j] < 0)
+                    ties_last = change.get("last_tie")
+                    if best is None or c < best[0] or (ties_last and c == best[0]):
+                        best = (c, i, j)
+            v = np.array(vals)
+            summ[b] = (v.mean(), v.std(ddof=1 if change.get("ddof1") else 0), best[0])
+            pairs[b] = (best[1], best[2], count)
+        return cos, summ, pairs
+    return fn
+
+
 @pytest.mark.parametrize("check,mutant", [
     (check_gram, _gram_off_by_one),
     (check_mgda_k2, _fw_swapped_pair),
@@ -570,6 +694,10 @@ def _combine_first_bucket_weights(x, offs, W):
     (check_pcgrad, _pcgrad_sign_flip),
     (check_cagrad, _cagrad_radius_squared),
     (check_combine, _combine_first_bucket_weights),
+    (check_conflicts, _conflicts_mutant(no_sqrt=True)),
+    (check_conflicts, _conflicts_mutant(le=True)),
+    (check_conflicts, _conflicts_mutant(last_tie=True)),
+    (check_conflicts, _conflicts_mutant(ddof1=True)),
 ])
 def test_planted_mistakes_are_caught(check, mutant):
     with pytest.raises(AssertionError):
