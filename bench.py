@@ -206,6 +206,18 @@ def main():
             st["combine"] += ev[2].elapsed_time(ev[3]) / args.steps
     log(f"{ms_step:.3f} ms/step; stages (ms) " + ", ".join(f"{k} {v:.3f}" for k, v in st.items()))
 
+    # per-bucket conflict diagnostics on the step's Gram matrices: outside the
+    # step (they read only the B*K*K Gram), timed on their own
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    bkmoo.conflicts(G)
+    e0.record(stream)
+    for _ in range(20):
+        bkmoo.conflicts(G)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    extras = {"conflicts": round(e0.elapsed_time(e1) / 20, 4)}
+    log(f"conflict diagnostics: {extras['conflicts'] * 1e3:.1f} us for {B} buckets")
+
     # dominant kernel: the resident kernel (reads K*s*N once, writes s*N), or
     # the longer of the two streaming passes
     if resident:
@@ -236,6 +248,7 @@ def main():
                    "method": wl.method, "max_iter": wl.max_iter, "cagrad_c": wl.cagrad_c},
         "path": "resident" if resident else "two-pass",
         "stages_ms": {k: round(v, 4) for k, v in st.items()},
+        "extras_ms": extras,
         "resolve_algorithmic_GBps": round((2 * K + 1) * s * N / (ms_step / 1e3) / 1e9, 1),
         "roofline": roof,
     }

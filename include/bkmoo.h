@@ -204,6 +204,34 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
                            hipStream_t stream);
 
 /*
+ * bkmoo_conflicts — per-bucket gradient-conflict diagnostics from Gram
+ * matrices.  Two task gradients conflict when their inner product (their
+ * cosine similarity) is negative (Section 2.1; the appendix definition of
+ * conflicting gradients); Figure 1 follows the mean and standard deviation
+ * of the pairwise cosines and counts a step as conflicting when some pair
+ * is negative.  Reads only `gram` (B*K*K*8 bytes), one thread per bucket,
+ * fp64, pairs i < j in lexicographic order.
+ *
+ *   gram     (in)  fp64 [B][K][K] (as written by bkmoo_gram / bkmoo_resolve)
+ *   cosines  (out, may be NULL) fp64 [B][K][K], symmetric:
+ *            G_ij / sqrt(G_ii G_jj) clipped to [-1, 1], 0 when either
+ *            gradient is zero; diagonal 1 (0 for a zero gradient)
+ *   summary  (out, may be NULL) fp64 [B][3]: mean, population standard
+ *            deviation and minimum of the K(K-1)/2 pairwise cosines
+ *   pairs    (out, may be NULL) int32 [B][3]: i, j (i < j) of the smallest
+ *            cosine, the first pair on ties; the number of pairs with
+ *            G_ij < 0 (> 0: the bucket has a conflict)
+ *
+ * A bucket whose Gram holds a NaN or infinity gets NaN cosines and summary
+ * and pairs (-1, -1, -1).  All pointers are device pointers owned by the
+ * caller; the call is asynchronous on `stream`.  BKMOO_EINVAL for K < 2,
+ * B < 1, a null `gram` or all three outputs null; BKMOO_EUNSUPPORTED for
+ * K > 16.
+ */
+bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *cosines,
+                             double *summary, int32_t *pairs, hipStream_t stream);
+
+/*
  * bkmoo_read_device_error — copy the workspace's device error word into
  * *err (host) after waiting for `stream`.  This call synchronises; it is a
  * diagnostic, not part of the hot path.  0 means the last call that used

@@ -50,6 +50,7 @@ def _load():
         "bkmoo_combine": [i32, vpp, ctypes.c_int, i64, i32, vp, vp, vp, ctypes.c_int, vp, sz, vp],
         "bkmoo_resolve": [i32, vpp, ctypes.c_int, i64, i32, vp, ctypes.c_int, ctypes.POINTER(_Hparams),
                           vp, ctypes.c_int, vp, vp, vp, vp, sz, vp],
+        "bkmoo_conflicts": [i32, i32, vp, vp, vp, vp, vp],
         "bkmoo_read_device_error": [vp, ctypes.POINTER(u32), vp],
         "bkmoo_set_grid_override": [i32],
         "bkmoo_resolve_path": [i32, i64, i32, ctypes.c_int, ctypes.c_int, i32, ctypes.c_int, i32,
@@ -68,7 +69,7 @@ def _load():
 _lib = _load()
 
 EXPORTS = ("bkmoo_workspace_size", "bkmoo_gram", "bkmoo_solve", "bkmoo_combine", "bkmoo_resolve",
-           "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
+           "bkmoo_conflicts", "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
            "bkmoo_set_resolve_path", "bkmoo_set_wait_limit", "bkmoo_status_string")
 
 
@@ -188,6 +189,25 @@ def solve(gram_in: torch.Tensor, method: str, max_iter: int = 20, cagrad_c: floa
     _check(_lib.bkmoo_solve(K, B, gram_in.data_ptr(), METHODS[method], ctypes.byref(hp),
                             weights.data_ptr(), aux.data_ptr(), _stream_ptr(dev)), "bkmoo_solve")
     return weights, aux
+
+
+def conflicts(gram_in: torch.Tensor, cosines: bool = True, summary: bool = True,
+              pairs: bool = True):
+    """Per-bucket conflict diagnostics from fp64 [B, K, K] Gram matrices:
+    (cosines fp64 [B, K, K], summary fp64 [B, 3] = mean / population std / min
+    pairwise cosine, pairs int32 [B, 3] = argmin pair and the count of pairs
+    with a negative inner product).  Outputs not asked for are None."""
+    if gram_in.dtype != torch.float64 or gram_in.dim() != 3 or not gram_in.is_contiguous():
+        raise ValueError("gram must be a contiguous fp64 [B, K, K] tensor")
+    B, K, _ = gram_in.shape
+    dev = gram_in.device
+    cos = torch.empty((B, K, K), dtype=torch.float64, device=dev) if cosines else None
+    summ = torch.empty((B, 3), dtype=torch.float64, device=dev) if summary else None
+    prs = torch.empty((B, 3), dtype=torch.int32, device=dev) if pairs else None
+    ptr = lambda t: t.data_ptr() if t is not None else None
+    _check(_lib.bkmoo_conflicts(K, B, gram_in.data_ptr(), ptr(cos), ptr(summ), ptr(prs),
+                                _stream_ptr(dev)), "bkmoo_conflicts")
+    return cos, summ, prs
 
 
 def combine(grads: Grads, bucket_offsets: torch.Tensor, weights: torch.Tensor,

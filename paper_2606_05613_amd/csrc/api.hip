@@ -92,6 +92,8 @@ struct Carved {
   double *gram;
   float *weights;
   double *partials;
+  int64_t *group_start;
+  double *groups;
   uint32_t *sync;
 };
 
@@ -100,7 +102,9 @@ Carved carve(void *ws, const Layout &L) {
   return Carved{reinterpret_cast<uint32_t *>(base + L.err),
                 reinterpret_cast<int64_t *>(base + L.chunk_start),
                 reinterpret_cast<double *>(base + L.gram), reinterpret_cast<float *>(base + L.weights),
-                reinterpret_cast<double *>(base + L.partials), reinterpret_cast<uint32_t *>(base + L.sync)};
+                reinterpret_cast<double *>(base + L.partials),
+                reinterpret_cast<int64_t *>(base + L.group_start),
+                reinterpret_cast<double *>(base + L.groups), reinterpret_cast<uint32_t *>(base + L.sync)};
 }
 
 // Workgroups for the resident path, or 0 when it should not be used.
@@ -164,12 +168,12 @@ bkmoo_status bkmoo_gram(int32_t K, const void *const *grads, bkmoo_dtype dt, int
   const Layout L = layout(K, N, B, dt);
   if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
   const Carved w = carve(workspace, L);
-  hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start, w.err,
-                                 nullptr, 0, stream);
+  hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start,
+                                 w.group_start, w.err, nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
-  const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec,
-                     g_grid_override.load()};
-  return hip_status(launch_gram(a, w.partials, gram, stream));
+  const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.group_start, w.err,
+                     shift, vec, g_grid_override.load()};
+  return hip_status(launch_gram(a, w.partials, w.groups, L.cap_groups, gram, stream));
 }
 
 bkmoo_status bkmoo_solve(int32_t K, int32_t B, const double *gram, bkmoo_method method,
@@ -199,10 +203,10 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
   const Carved w = carve(workspace, L);
   hipError_t e = launch_schedule(bucket_offsets, B, N, combine_chunk_elems(K, dt), w.chunk_start,
-                                 w.err, nullptr, 0, stream);
+                                 nullptr, w.err, nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
-  const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec,
-                     g_grid_override.load()};
+  const StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, nullptr, w.err, shift,
+                     vec, g_grid_override.load()};
   return hip_status(launch_combine(a, weights, out, (int)out_dt, stream));
 }
 
@@ -232,7 +236,7 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   const int rgrid = choose_resident(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters);
   if (rgrid > 0) {
     hipError_t e = launch_schedule(bucket_offsets, B, N, resident_segment_elems(K, dt), w.chunk_start,
-                                   w.err, w.sync, 2 * (int64_t)B, stream);
+                                   nullptr, w.err, w.sync, 2 * (int64_t)B, stream);
     if (e != hipSuccess) return BKMOO_EHIP;
     e = launch_resident(K, (int)dt, (int)out_dt, grads, bucket_offsets, w.chunk_start, B, shift,
                         (int)method, iters, c, order, G, W, aux, out, w.partials, w.sync, w.sync + B,
@@ -240,21 +244,30 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
     return hip_status(e);
   }
 
-  hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start, w.err,
-                                 nullptr, 0, stream);
+  hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start,
+                                 w.group_start, w.err, nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
-  StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.err, shift, vec_in,
-               g_grid_override.load()};
-  if ((e = launch_gram(a, w.partials, G, stream)) != hipSuccess) return BKMOO_EHIP;
+  StreamArgs a{K, (int)dt, grads, N, B, bucket_offsets, w.chunk_start, w.group_start, w.err, shift,
+               vec_in, g_grid_override.load()};
+  if ((e = launch_gram(a, w.partials, w.groups, L.cap_groups, G, stream)) != hipSuccess)
+    return BKMOO_EHIP;
   if ((e = launch_solve(K, B, G, (int)method, iters, c, order, W, aux, stream)) != hipSuccess)
     return BKMOO_EHIP;
   // the combine pass cuts its own chunks (the schedule keeps the error word
   // the Gram pass's schedule set: offsets are the same)
-  e = launch_schedule(bucket_offsets, B, N, combine_chunk_elems(K, dt), w.chunk_start, w.err, nullptr,
-                      0, stream);
+  e = launch_schedule(bucket_offsets, B, N, combine_chunk_elems(K, dt), w.chunk_start, nullptr, w.err,
+                      nullptr, 0, stream);
   if (e != hipSuccess) return BKMOO_EHIP;
   a.vec = vec_out;
   return hip_status(launch_combine(a, W, out, (int)out_dt, stream));
+}
+
+bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *cosines,
+                             double *summary, int32_t *pairs, hipStream_t stream) {
+  if (K < kMinK || B < 1) return BKMOO_EINVAL;
+  if (K > kMaxK) return BKMOO_EUNSUPPORTED;
+  if (!gram || (!cosines && !summary && !pairs)) return BKMOO_EINVAL;
+  return hip_status(launch_conflicts(K, B, gram, cosines, summary, pairs, stream));
 }
 
 bkmoo_status bkmoo_read_device_error(const void *workspace, uint32_t *err, hipStream_t stream) {

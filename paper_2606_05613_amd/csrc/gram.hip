@@ -12,9 +12,11 @@
 // non-temporal loads per iteration and accumulates all K(K+1)/2 products
 // in fp32 registers over the chunk's iterations.  Lane sums are combined by
 // a fixed xor butterfly across the wavefront, then in fp64 across the 4
-// wavefronts through LDS in wave order, and land in a per-chunk slot.  A finalize kernel adds
-// a bucket's chunk slots in chunk order.  No atomics: the result is
-// bitwise independent of the grid and of scheduling.
+// wavefronts through LDS in wave order, and land in a per-chunk slot.  Two
+// finalize kernels add a bucket's chunk slots in fp64 in an order fixed by
+// the bucket's chunk count (groups of consecutive chunks, then the groups in
+// order).  No atomics: the result is bitwise independent of the grid and of
+// scheduling.
 #include "stream_common.h"
 
 namespace bkmoo {
@@ -130,19 +132,44 @@ __global__ __launch_bounds__(kThreads) void gram_partial_kernel(
   }
 }
 
-// One wavefront per bucket: add the bucket's chunk slots in chunk order and
-// write the symmetric K x K matrix (NaN everywhere when the offsets were
-// rejected by the schedule).
+// Finalize, level 1: one workgroup per group of up to kFinalizeGroup
+// consecutive chunks of one bucket (grid-stride over the groups).  Wavefront
+// w handles the pairs p = w, w + 4, ...; lane l adds the group's chunks l,
+// l + 64, l + 128, ... in that order in fp64, then a fixed xor butterfly adds
+// the 64 lane sums.  The order depends only on the group's chunk count.
+__global__ __launch_bounds__(kThreads) void gram_group_kernel(
+    int K, int B, const int64_t *__restrict__ cs, const int64_t *__restrict__ gs,
+    const double *__restrict__ partials, double *__restrict__ groups) {
+  const int P = K * (K + 1) / 2;
+  const int64_t total = gs[B];
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  for (int64_t v = blockIdx.x; v < total; v += gridDim.x) {
+    const int b = find_bucket(gs, B, v);
+    const int64_t c_lo = cs[b] + (v - gs[b]) * kFinalizeGroup;
+    const int64_t c_end = c_lo + kFinalizeGroup < cs[b + 1] ? c_lo + kFinalizeGroup : cs[b + 1];
+    for (int p = wave; p < P; p += kThreads / kWave) {
+      double s = 0.0;
+      for (int64_t c = c_lo + lane; c < c_end; c += kWave) s += partials[c * P + p];
+#pragma unroll
+      for (int off = kWave / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, kWave);
+      if (lane == 0) groups[v * P + p] = s;
+    }
+  }
+}
+
+// Finalize, level 2: one wavefront per bucket adds the bucket's group sums in
+// group order and writes the symmetric K x K matrix (NaN everywhere when the
+// offsets were rejected by the schedule).
 __global__ __launch_bounds__(kWave) void gram_finalize_kernel(
-    int K, const int64_t *__restrict__ cs, const double *__restrict__ partials,
+    int K, const int64_t *__restrict__ gs, const double *__restrict__ groups,
     const uint32_t *__restrict__ err, double *__restrict__ gram) {
   const int b = blockIdx.x;
   const int P = K * (K + 1) / 2;
   const bool bad = (*err & kErrOffsets) != 0u;
-  const int64_t c0 = cs[b], c1 = cs[b + 1];
+  const int64_t g0 = gs[b], g1 = gs[b + 1];
   for (int p = threadIdx.x; p < P; p += kWave) {
     double s = 0.0;
-    for (int64_t c = c0; c < c1; ++c) s += partials[c * P + p];
+    for (int64_t g = g0; g < g1; ++g) s += groups[g * P + p];
     if (bad) s = __builtin_nan("");
     int i = 0, rem = p;
     while (rem >= K - i) {
@@ -195,11 +222,17 @@ hipError_t dispatch_gram(const StreamArgs &a, double *partials, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_gram(const StreamArgs &a, double *partials, double *gram, hipStream_t s) {
+hipError_t launch_gram(const StreamArgs &a, double *partials, double *groups, int64_t cap_groups,
+                       double *gram, hipStream_t s) {
   hipError_t e = a.dt == F32 ? dispatch_gram<F32>(a, partials, s) : dispatch_gram<BF16>(a, partials, s);
   if (e != hipSuccess) return e;
+  const int64_t limit = (int64_t)device_cu_count() * 8;
+  const int64_t ggrid = cap_groups < limit ? cap_groups : limit;
+  hipLaunchKernelGGL(gram_group_kernel, dim3((unsigned)(ggrid > 0 ? ggrid : 1)), dim3(kThreads), 0, s,
+                     a.K, a.B, a.chunk_start, a.group_start, partials, groups);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(gram_finalize_kernel, dim3((unsigned)a.B), dim3(kWave), 0, s, a.K,
-                     a.chunk_start, partials, a.err, gram);
+                     a.group_start, groups, a.err, gram);
   return hipGetLastError();
 }
 

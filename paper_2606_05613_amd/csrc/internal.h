@@ -40,16 +40,23 @@ constexpr int64_t combine_chunk_elems(int K, int dt) { return shape_elems(combin
 
 constexpr int pairs(int K) { return K * (K + 1) / 2; }
 
+// The Gram finalize adds a bucket's chunk slots in groups of this many
+// consecutive chunks (one workgroup per group), then the group sums in group
+// order: the summation order depends only on the bucket's chunk count.
+constexpr int kFinalizeGroup = 1024;
+
 // Workspace layout (every region 256-byte aligned):
 //   [0, 256)            header: uint32 error word at byte 0
 //   chunk_start         int64 [B + 1]     (prefix sum of chunks per bucket)
 //   gram                fp64  [B][K][K]   (used when the caller passes none)
 //   weights             fp32  [B][K]      (used when the caller passes none)
 //   partials            fp64  [cap][P]    cap = ceil(N / C) + B
+//   group_start         int64 [B + 1]     (prefix sum of finalize groups per bucket)
+//   groups              fp64  [gcap][P]   gcap = cap / kFinalizeGroup + B + 1
 //   sync                uint32 [2][B]     resident path: arrival counters, flags
 struct Layout {
-  size_t err, chunk_start, gram, weights, partials, sync, total;
-  int64_t cap_chunks;
+  size_t err, chunk_start, gram, weights, partials, group_start, groups, sync, total;
+  int64_t cap_chunks, cap_groups;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -64,6 +71,9 @@ inline Layout layout(int K, int64_t N, int B, int dt) {
   L.gram = o;           o = align256(o + sizeof(double) * (size_t)B * K * K);
   L.weights = o;        o = align256(o + sizeof(float) * (size_t)B * K);
   L.partials = o;       o = align256(o + sizeof(double) * (size_t)L.cap_chunks * pairs(K));
+  L.cap_groups = L.cap_chunks / kFinalizeGroup + B + 1;
+  L.group_start = o;    o = align256(o + sizeof(int64_t) * (size_t)(B + 1));
+  L.groups = o;         o = align256(o + sizeof(double) * (size_t)L.cap_groups * pairs(K));
   L.sync = o;           o = align256(o + sizeof(uint32_t) * 2 * (size_t)B);
   L.total = o;
   return L;
@@ -88,21 +98,29 @@ struct StreamArgs {
   int B;
   const int64_t *offsets;      // device [B+1]
   const int64_t *chunk_start;  // device [B+1] (from the schedule kernel)
+  const int64_t *group_start;  // device [B+1] finalize groups (Gram pass only)
   const uint32_t *err;         // device error word
   int shift;                   // rows are 16-byte aligned at element n = shift (mod V)
   bool vec;                    // 128-bit path allowed
   int grid;                    // workgroups (0: automatic)
 };
 
-// Validates offsets, writes chunk_start for chunks of C elements, clears the
-// error word and zeroes `nsync` words at `sync` (may be null).
+// Validates offsets, writes chunk_start for chunks of C elements (and, if
+// group_start is not null, the prefix of finalize groups), clears the error
+// word and zeroes `nsync` words at `sync` (may be null).
 hipError_t launch_schedule(const int64_t *offsets, int B, int64_t N, int64_t C, int64_t *chunk_start,
-                           uint32_t *err, uint32_t *sync, int64_t nsync, hipStream_t s);
-hipError_t launch_gram(const StreamArgs &a, double *partials, double *gram, hipStream_t s);
+                           int64_t *group_start, uint32_t *err, uint32_t *sync, int64_t nsync,
+                           hipStream_t s);
+// Gram pass: per-chunk partials, group sums, then the per-bucket matrices.
+// `cap_groups` bounds the number of finalize groups (sizes the group grid).
+hipError_t launch_gram(const StreamArgs &a, double *partials, double *groups, int64_t cap_groups,
+                       double *gram, hipStream_t s);
 hipError_t launch_solve(int K, int B, const double *gram, int method, int max_iter, double c,
                         const int8_t *order, float *weights, double *aux, hipStream_t s);
 hipError_t launch_combine(const StreamArgs &a, const float *weights, void *out, int out_dt,
                           hipStream_t s);
+hipError_t launch_conflicts(int K, int B, const double *gram, double *cosines, double *summary,
+                            int32_t *pairs, hipStream_t s);
 
 // Single-read resident resolve (K <= 4): elements per segment, workgroups
 // of the cooperative launch (0 if the combination cannot run resident).

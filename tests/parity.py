@@ -20,6 +20,13 @@ Tolerances (written here once, used by every parity test):
     - end to end: ||gpu - d|| <= ||round(d) - d|| + 1e-4 ||d|| with d the
       oracle's float64 update from its own weights (the output type's own
       rounding is unavoidable and is not counted against the path).
+* Conflict diagnostics: from the same Gram, cosines within 1e-15 and the
+  summary within 1e-14 (fp64, only the summation order differs), counts
+  exact, the argmin pair exact when the smallest cosine is unique by more
+  than 1e-14 (else the GPU's pair must attain the minimum); end to end
+  (GPU Gram vs exact Gram) cosines and summary within 3 tau, since a Gram
+  error of tau sqrt(G_ii G_jj) moves a cosine by at most ~2 tau, and signs
+  compared only on pairs with |cos| > 3 tau.
 """
 
 from __future__ import annotations
@@ -164,3 +171,39 @@ def full_parity(lib, wl, grads=None, out_dtype=None):
     e_o = assert_out(host_out(res["out"]), x64, offs_np, res["weights"], ora["weights"], odt,
                      where=wl.name)
     return {"gram": e_g, "w_iso": e_wi, "w_e2e": e_we, "out_iso": e_o[0], "out_e2e": e_o[1]}
+
+
+def assert_conflicts(got, want, where="", tol_cos=1e-15, tol_sum=1e-14, sign_margin=None):
+    """Compare (cos, summary, pairs) from the GPU with the oracle's.  With
+    `sign_margin` (end to end) the pair statistics are compared only where
+    the exact cosine is farther than the margin from 0 or from a tie."""
+    cos_g, sum_g, pr_g = (np.asarray(t) for t in got)
+    cos_o, sum_o, pr_o = (np.asarray(t) for t in want)
+    nb, k, _ = cos_o.shape
+    bad = ~np.isfinite(cos_o).all(axis=(1, 2))
+    assert np.array_equal(bad, ~np.isfinite(cos_g).all(axis=(1, 2))), where
+    assert np.all(pr_g[bad] == -1) and np.all(np.isnan(sum_g[bad])), where
+    ok = ~bad
+    dc = np.abs(cos_g[ok] - cos_o[ok]).max() if ok.any() else 0.0
+    assert dc <= tol_cos, f"{where}: cosines differ by {dc:.3e} > {tol_cos:.1e}"
+    ds = np.abs(sum_g[ok] - sum_o[ok]).max() if ok.any() else 0.0
+    assert ds <= tol_sum, f"{where}: summary differs by {ds:.3e} > {tol_sum:.1e}"
+    iu = np.triu_indices(k, 1)
+    for b in np.nonzero(ok)[0]:
+        vals = cos_o[b][iu]
+        i, j = int(pr_g[b, 0]), int(pr_g[b, 1])
+        assert 0 <= i < j < k, f"{where} bucket {b}: invalid pair {(i, j)}"
+        assert abs(cos_o[b, i, j] - sum_o[b, 2]) <= tol_sum + 2 * tol_cos, \
+            f"{where} bucket {b}: pair {(i, j)} does not attain the minimum"
+        gap = np.sort(vals)[1] - vals.min() if len(vals) > 1 else np.inf
+        if gap > tol_sum + 2 * tol_cos:
+            assert (i, j) == (int(pr_o[b, 0]), int(pr_o[b, 1])), f"{where} bucket {b}: argmin pair"
+        if sign_margin is None:
+            assert pr_g[b, 2] == pr_o[b, 2], f"{where} bucket {b}: conflict count"
+        else:
+            clear = np.abs(vals) > sign_margin
+            neg_g = (cos_g[b][iu] < 0)[clear]
+            neg_o = (vals < 0)[clear]
+            assert np.array_equal(neg_g, neg_o), f"{where} bucket {b}: conflict signs"
+            if clear.all():
+                assert pr_g[b, 2] == pr_o[b, 2], f"{where} bucket {b}: conflict count"

@@ -112,6 +112,16 @@ def test_solve_and_resolve_hparam_errors(b):
                            ws_need - 1, None) == -3
 
 
+def test_conflicts_argument_errors(b):
+    L = b._lib
+    g, o = FAKE, FAKE + (1 << 20)
+    assert L.bkmoo_conflicts(1, 3, g, o, None, None, None) == -1       # K < 2
+    assert L.bkmoo_conflicts(17, 3, g, o, None, None, None) == -2      # K > 16
+    assert L.bkmoo_conflicts(4, 0, g, o, None, None, None) == -1       # no bucket
+    assert L.bkmoo_conflicts(4, 3, None, o, None, None, None) == -1    # no Gram
+    assert L.bkmoo_conflicts(4, 3, g, None, None, None, None) == -1    # no output
+
+
 def test_grid_override_rejects_negative(b):
     assert b._lib.bkmoo_set_grid_override(-1) == -1
     assert b._lib.bkmoo_set_grid_override(0) == 0

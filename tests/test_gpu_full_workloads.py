@@ -9,7 +9,11 @@ At these sizes the oracle cannot redo everything, so each workload checks:
 * 100k seeded element positions spread over all N: the update element
   against the exactly computed weighted sum of the GPU weights (bf16 output:
   the correctly rounded value; fp32 output: within K fp32 ulps of the sum
-  of magnitudes).
+  of magnitudes);
+* conflict diagnostics: every bucket against the oracle on the GPU's Gram,
+  sampled buckets against the oracle's Gram, and, for the unit-scale
+  normal workloads, every bucket's cosines against the correlation matrix
+  the gradients were drawn with (sampling error ~1/sqrt(n_b) ~ 3e-4).
 """
 
 import gc
@@ -20,7 +24,8 @@ import torch
 
 import oracle
 from synth import WORKLOADS, fill_grads, host_rows
-from tests.parity import assert_gram, assert_out, assert_weights, run_resolve, singular_buckets
+from tests.parity import TAU, assert_conflicts, assert_gram, assert_out, assert_weights, run_resolve, \
+    singular_buckets
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -42,6 +47,23 @@ def _check_workload(lib, wl, grads, offs, order):
     if wl.method in ("mgda", "cagrad"):
         a = res["aux"]
         assert a.min() >= -1e-12 and np.abs(a.sum(1) - 1).max() <= 1e-9
+    # conflict diagnostics on the GPU Gram, every bucket
+    conf = [t.cpu().numpy() for t in lib.conflicts(torch.from_numpy(res["gram"]).to(grads.device))]
+    assert_conflicts(conf, oracle.conflicts(res["gram"]), f"{wl.name} conflicts(iso)")
+    if wl.dist == "normal" and wl.tensor_scale is None and wl.task_scale is None:
+        C = wl.correlations()
+        iu = np.triu_indices(wl.K, 1)
+        rho = C[:, iu[0], iu[1]]
+        n_b = np.maximum(np.diff(wl.offsets()), 1)[:, None]
+        bound = 8 * (1 - rho ** 2) / np.sqrt(n_b) + 1e-3      # 8 sigma of a sample correlation
+        err = np.abs(conf[0][:, iu[0], iu[1]] - rho)
+        dev = err.max()
+        assert np.all(err <= bound), f"{wl.name}: cosines {dev:.2e} away from the drawn correlations"
+        clear = (np.abs(rho) > bound).all(axis=1)
+        neg = (C[:, iu[0], iu[1]] < 0).sum(axis=1)
+        assert np.array_equal(conf[2][clear, 2], neg[clear]), f"{wl.name}: conflict counts"
+        print(f"  conflicts: {int((conf[2][:, 2] > 0).sum())} of {wl.B} buckets, max |cos - C| {dev:.1e}",
+              flush=True)
     # sampled buckets end to end
     offs_np = wl.offsets()
     rng = np.random.default_rng(wl.seed)
@@ -53,6 +75,10 @@ def _check_workload(lib, wl, grads, offs, order):
         ora = oracle.resolve(rows, ob, wl.method, max_iter=wl.max_iter, cagrad_c=wl.cagrad_c,
                              orders=None if orders_np is None else orders_np[b:b + 1])
         assert_gram(res["gram"][b:b + 1], ora["gram"], wl.dtype, f"{wl.name} bucket {b}")
+        tau = TAU[wl.dtype]
+        assert_conflicts([c[b:b + 1] for c in conf], oracle.conflicts(ora["gram"]),
+                         f"{wl.name} bucket {b} conflicts(e2e)", tol_cos=3 * tau, tol_sum=3 * tau,
+                         sign_margin=3 * tau)
         skip = singular_buckets(ora["gram"]) if wl.method in ("mgda", "cagrad") else None
         assert_weights(res["weights"][b:b + 1], ora["weights"], "weights(e2e)", f"{wl.name} bucket {b}",
                        skip=skip)
