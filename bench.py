@@ -46,10 +46,19 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_source_sha() -> str:
+# The sources each timed kernel is compiled from (its file and the headers it
+# includes): a committed counter summary applies while these are unchanged.
+KERNEL_SOURCES = {
+    "gram": ["gram.hip", "stream_common.h", "internal.h"],
+    "combine": ["combine.hip", "combine_impl.h", "stream_common.h", "internal.h"],
+    "resident": ["resident.hip", "combine_impl.h", "solve_impl.h", "stream_common.h", "internal.h"],
+}
+
+
+def kernel_source_sha(kernel: str) -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_05613_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in KERNEL_SOURCES[kernel]:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode())
             h.update(fh.read())
@@ -65,7 +74,7 @@ def committed_traffic(workload: str, kernel: str):
     text = open(path).read()
     sha = re.search(r"source_sha:\s*(\w+)", text)
     val = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not sha or not val or sha.group(1) != kernel_source_sha():
+    if not sha or not val or sha.group(1) != kernel_source_sha(kernel):
         return None
     return float(val.group(1))
 
