@@ -227,6 +227,28 @@ def main():
     extras = {"conflicts": round(e0.elapsed_time(e1) / 20, 4)}
     log(f"conflict diagnostics: {extras['conflicts'] * 1e3:.1f} us for {B} buckets")
 
+    # the exact solvers (support enumeration) on the step's Gram matrices, and
+    # at their heaviest scope: K=10 with 6,564 buckets (1 MiB fp32 buckets of
+    # a 1.7B-parameter model), on seeded random positive definite Grams
+    def time_solve(g, method, reps=5):
+        bkmoo.solve(g, method, cagrad_c=wl.cagrad_c)
+        e0.record(stream)
+        for _ in range(reps):
+            bkmoo.solve(g, method, cagrad_c=wl.cagrad_c)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return round(e0.elapsed_time(e1) / reps, 4)
+
+    if K <= 10:
+        extras["solve_mgda_exact"] = time_solve(G, "mgda-exact")
+        extras["solve_cagrad_exact"] = time_solve(G, "cagrad-exact")
+    gen = torch.Generator(device=dev).manual_seed(1005)
+    x10 = torch.randn((6564, 10, 24), generator=gen, device=dev, dtype=torch.float64)
+    G10 = torch.matmul(x10, x10.transpose(1, 2).contiguous()).contiguous()
+    extras["solve_mgda_exact_k10_b6564"] = time_solve(G10, "mgda-exact", reps=2)
+    extras["solve_cagrad_exact_k10_b6564"] = time_solve(G10, "cagrad-exact", reps=2)
+    log("exact solvers (ms): " + ", ".join(f"{k} {v:.3f}" for k, v in extras.items() if "exact" in k))
+
     # dominant kernel: the resident kernel (reads K*s*N once, writes s*N), or
     # the longer of the two streaming passes
     if resident:

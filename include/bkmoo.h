@@ -77,7 +77,9 @@ typedef enum {
   BKMOO_MGDA = 0,    /* min-norm point of the bucket's gradient hull, Eq. (shard-mgda) */
   BKMOO_PCGRAD = 1,  /* projection of conflicting pairs, Eq. (pcgrad_proj), Algorithm 1 */
   BKMOO_CAGRAD = 2,  /* conflict-averse direction in a ball around the mean, Eq. (cagrad) */
-  BKMOO_MEAN = 3     /* averaged gradient (1/K) sum_i x_i, Section 2.1 */
+  BKMOO_MEAN = 3,    /* averaged gradient (1/K) sum_i x_i, Section 2.1 */
+  BKMOO_MGDA_EXACT = 4,   /* MGDA's min-norm point solved exactly (K <= 10) */
+  BKMOO_CAGRAD_EXACT = 5  /* CAGrad's dual solved exactly (K <= 10) */
 } bkmoo_method;
 
 /* Device error word bits (bkmoo_read_device_error). */
@@ -154,7 +156,25 @@ bkmoo_status bkmoo_gram(int32_t K, const void *const *grads, bkmoo_dtype dt, int
  *          d = g_avg + c||g_avg|| g_w/||g_w||, i.e. weights = 1/K + r w/||g_w||
  *          (1/K when r = 0 or g_w vanishes); aux = w.
  *   MEAN   weights = aux = 1/K.
- * `hp` (host) may be NULL for MEAN; PCGrad ignores max_iter and c.
+ *   MGDA_EXACT / CAGRAD_EXACT  the same two problems solved exactly, K <= 10,
+ *          by enumerating the 2^K - 1 supports S (one wavefront per bucket,
+ *          one support per lane at a time, Gaussian elimination with partial
+ *          pivoting per support; a support with an exactly zero pivot is
+ *          skipped).  Supports are ranked by size, then lexicographically.
+ *          MGDA: on S, G_SS a = mu 1 with 1^T a = 1 (G divided by its largest
+ *          diagonal entry); kept if a >= -1e-10, |1^T a - 1| <= 1e-9 and,
+ *          clipped and renormalised, (G a)_t >= a^T G a - 1e-9 for every t;
+ *          the first kept support in rank order wins unless a later one is
+ *          lower by more than 1e-12; none kept -> 5000 Frank-Wolfe
+ *          iterations.  weights = aux = alpha.  CAGrad: the vertices and, for
+ *          r > 0 and |S| >= 2, both roots of the stationarity conditions on
+ *          S (v_S = G_SS^-1 (lam 1 - b_S) / r with v^T G v = 1), kept if
+ *          v >= -1e-12 and 1^T v > 0, normalised onto the simplex; least dual
+ *          value wins, first in rank order on ties (vertices, then supports,
+ *          smaller root first); weights and aux as for CAGRAD.  max_iter is
+ *          ignored; CAGRAD_EXACT needs hp->cagrad_c.
+ * `hp` (host) may be NULL for MEAN and MGDA_EXACT; PCGrad ignores max_iter
+ * and c.  BKMOO_EUNSUPPORTED for an exact method with K > 10.
  */
 bkmoo_status bkmoo_solve(int32_t K, int32_t B, const double *gram, bkmoo_method method,
                          const bkmoo_hparams *hp, float *weights, double *aux, hipStream_t stream);

@@ -22,7 +22,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libbkmoo.so")
 
 F32, BF16 = 0, 1
-METHODS = {"mgda": 0, "pcgrad": 1, "cagrad": 2, "mean": 3}
+METHODS = {"mgda": 0, "pcgrad": 1, "cagrad": 2, "mean": 3, "mgda-exact": 4, "cagrad-exact": 5}
 DEVERR_OFFSETS = 0x1
 DEVERR_TIMEOUT = 0x2
 PATH_TWO_PASS, PATH_RESIDENT = 1, 2

@@ -32,10 +32,10 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libbkmoo.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.hip", "schedule.hip", "gram.hip", "solve.hip", "combine.hip", "resident.hip",
-           "conflicts.hip"]
-EXTRA = {"solve.hip": ["-ffp-contract=off"], "resident.hip": ["-ffp-contract=off"],
-         "conflicts.hip": ["-ffp-contract=off"]}
+SOURCES = ["api.hip", "schedule.hip", "gram.hip", "solve.hip", "solve_exact.hip", "combine.hip",
+           "resident.hip", "conflicts.hip"]
+EXTRA = {"solve.hip": ["-ffp-contract=off"], "solve_exact.hip": ["-ffp-contract=off"],
+         "resident.hip": ["-ffp-contract=off"], "conflicts.hip": ["-ffp-contract=off"]}
 
 
 def hipcc() -> str:

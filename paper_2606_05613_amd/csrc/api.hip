@@ -75,14 +75,22 @@ bkmoo_status check_out(int32_t K, const void *const *grads, int dt, int64_t N, c
   return BKMOO_OK;
 }
 
+bool is_exact(int method) { return method == BKMOO_MGDA_EXACT || method == BKMOO_CAGRAD_EXACT; }
+
 bkmoo_status check_hparams(int method, const bkmoo_hparams *hp) {
-  if (method < BKMOO_MGDA || method > BKMOO_MEAN) return BKMOO_EINVAL;
-  if (method == BKMOO_MEAN) return BKMOO_OK;
+  if (method < BKMOO_MGDA || method > BKMOO_CAGRAD_EXACT) return BKMOO_EINVAL;
+  if (method == BKMOO_MEAN || method == BKMOO_MGDA_EXACT) return BKMOO_OK;
   if (!hp) return BKMOO_EINVAL;
-  if (method != BKMOO_PCGRAD && (hp->max_iter < 0 || hp->max_iter > 1000000)) return BKMOO_EINVAL;
-  if (method == BKMOO_CAGRAD && !(hp->cagrad_c >= 0.0 && hp->cagrad_c < 1.0)) return BKMOO_EINVAL;
+  if ((method == BKMOO_MGDA || method == BKMOO_CAGRAD) && (hp->max_iter < 0 || hp->max_iter > 1000000))
+    return BKMOO_EINVAL;
+  if ((method == BKMOO_CAGRAD || method == BKMOO_CAGRAD_EXACT) &&
+      !(hp->cagrad_c >= 0.0 && hp->cagrad_c < 1.0))
+    return BKMOO_EINVAL;
   return BKMOO_OK;
 }
+
+// K beyond what the method supports (exact solvers enumerate 2^K - 1 supports).
+bool k_unsupported(int K, int method) { return K > kMaxK || (is_exact(method) && K > kExactMaxK); }
 
 bkmoo_status hip_status(hipError_t e) { return e == hipSuccess ? BKMOO_OK : BKMOO_EHIP; }
 
@@ -110,7 +118,7 @@ Carved carve(void *ws, const Layout &L) {
 // Workgroups for the resident path, or 0 when it should not be used.
 int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters) {
   const int mode = g_resolve_path.load();
-  if (mode == 1 || K > 4 || !vec) return 0;
+  if (mode == 1 || K > 4 || !vec || is_exact(method)) return 0;
   static std::atomic<int> cache[3][2][2];  // K-2, dt, out_dt (device model is fixed per process here)
   int g = cache[K - 2][dt][out_dt].load();
   if (g == 0) {
@@ -183,6 +191,7 @@ bkmoo_status bkmoo_solve(int32_t K, int32_t B, const double *gram, bkmoo_method 
   if (!gram || !weights) return BKMOO_EINVAL;
   const bkmoo_status st = check_hparams(method, hp);
   if (st != BKMOO_OK) return st;
+  if (k_unsupported(K, method)) return BKMOO_EUNSUPPORTED;
   const int iters = hp ? hp->max_iter : 0;
   const double c = hp ? hp->cagrad_c : 0.0;
   const int8_t *order = hp ? hp->pcgrad_order : nullptr;
@@ -223,6 +232,7 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   bool vec_out = vec_in;
   if ((st = check_out(K, grads, dt, N, out, out_dt, shift, &vec_out)) != BKMOO_OK) return st;
   if ((st = check_hparams(method, hp)) != BKMOO_OK) return st;
+  if (k_unsupported(K, method)) return BKMOO_EUNSUPPORTED;
   if (!bucket_offsets || !workspace) return BKMOO_EINVAL;
   const Layout L = layout(K, N, B, dt);
   if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
@@ -292,7 +302,8 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
   if (!path) return BKMOO_EINVAL;
   const bkmoo_status st = check_shape(K, N, B, dt);
   if (st != BKMOO_OK) return st;
-  if (!valid_dtype(out_dt) || method < BKMOO_MGDA || method > BKMOO_MEAN) return BKMOO_EINVAL;
+  if (!valid_dtype(out_dt) || method < BKMOO_MGDA || method > BKMOO_CAGRAD_EXACT) return BKMOO_EINVAL;
+  if (k_unsupported(K, method)) return BKMOO_EUNSUPPORTED;
   *path = choose_resident(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter) > 0
               ? BKMOO_PATH_RESIDENT
               : BKMOO_PATH_TWO_PASS;

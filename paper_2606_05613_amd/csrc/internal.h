@@ -9,6 +9,7 @@ namespace bkmoo {
 
 constexpr int kMinK = 2;
 constexpr int kMaxK = 16;
+constexpr int kExactMaxK = 10;  // exact solvers: 2^K - 1 supports per bucket
 constexpr int kThreads = 256;          // streaming kernels: 4 wavefronts of 64
 constexpr int kWave = 64;
 
@@ -121,6 +122,9 @@ hipError_t launch_combine(const StreamArgs &a, const float *weights, void *out, 
                           hipStream_t s);
 hipError_t launch_conflicts(int K, int B, const double *gram, double *cosines, double *summary,
                             int32_t *pairs, hipStream_t s);
+// Exact MGDA / CAGrad solvers by support enumeration (K <= kExactMaxK).
+hipError_t launch_exact_solve(int K, int B, const double *gram, int method, double c, float *weights,
+                              double *aux, hipStream_t s);
 
 // Single-read resident resolve (K <= 4): elements per segment, workgroups
 // of the cooperative launch (0 if the combination cannot run resident).

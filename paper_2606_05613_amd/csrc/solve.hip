@@ -31,6 +31,8 @@ __global__ __launch_bounds__(kWave) void solve_kernel(int K, const double *__res
 
 hipError_t launch_solve(int K, int B, const double *gram, int method, int max_iter, double c,
                         const int8_t *order, float *weights, double *aux, hipStream_t s) {
+  if (method == MGDA_EXACT || method == CAGRAD_EXACT)
+    return launch_exact_solve(K, B, gram, method, c, weights, aux, s);
   hipLaunchKernelGGL(solve_kernel, dim3((unsigned)B), dim3(kWave), 0, s, K, gram, method, max_iter,
                      c, order, weights, aux);
   return hipGetLastError();

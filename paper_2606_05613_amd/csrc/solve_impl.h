@@ -26,7 +26,7 @@ struct WaveSync {
   }
 };
 
-enum Method : int { MGDA = 0, PCGRAD = 1, CAGRAD = 2, MEAN = 3 };
+enum Method : int { MGDA = 0, PCGRAD = 1, CAGRAD = 2, MEAN = 3, MGDA_EXACT = 4, CAGRAD_EXACT = 5 };
 
 // min over gamma in [0, 1] of |gamma a + (1 - gamma) b|^2 from aa, ab, bb
 // (Eq. mgda restricted to a segment): the stationary point
@@ -137,6 +137,28 @@ __device__ void solve_pcgrad(Shared &S, int K, const int8_t *order, int64_t b, i
   Sync()();
 }
 
+// CAGrad's primal weights from the dual point w = S.a: d = g_avg + r g_w /
+// |g_w|, i.e. weights 1/K + (r / |g_w|) w_t, or 1/K when r = 0 or g_w
+// vanishes relative to the largest gradient.  Writes S.C[0..K).
+template <typename Sync>
+__device__ void cagrad_primal(Shared &S, int K, double r, double invK, int t) {
+  if (t < K) {
+    double s = 0.0;
+    for (int j = 0; j < K; ++j) s += S.G[t * K + j] * S.a[j];
+    S.v[t] = s;
+  }
+  Sync()();
+  double q = 0.0, dmax = 0.0;
+  for (int i = 0; i < K; ++i) q += S.a[i] * S.v[i];
+  for (int i = 0; i < K; ++i) dmax = S.G[i * K + i] > dmax ? S.G[i * K + i] : dmax;
+  const double nrm = sqrt(q > 0.0 ? q : 0.0);
+  const double scale = sqrt(dmax);
+  const bool degenerate = r == 0.0 || nrm <= 1e-12 * scale || nrm == 0.0;
+  Sync()();
+  if (t < K) S.C[t] = degenerate ? invK : invK + (r / nrm) * S.a[t];  // weights
+  Sync()();
+}
+
 // CAGrad through its dual min_{w in simplex} F(w) = b^T w + r sqrt(w^T G w)
 // (b = G 1 / K, r = c |g_avg|), Frank-Wolfe from the uniform point with an
 // exact line search; primal d = g_avg + r g_w / |g_w|.
@@ -217,22 +239,7 @@ __device__ void solve_cagrad(Shared &S, int K, int iters, double c, int t) {
     }
     Sync()();
   }
-  // primal weights
-  if (t < K) {
-    double s = 0.0;
-    for (int j = 0; j < K; ++j) s += S.G[t * K + j] * S.a[j];
-    S.v[t] = s;
-  }
-  Sync()();
-  double q = 0.0, dmax = 0.0;
-  for (int i = 0; i < K; ++i) q += S.a[i] * S.v[i];
-  for (int i = 0; i < K; ++i) dmax = S.G[i * K + i] > dmax ? S.G[i * K + i] : dmax;
-  const double nrm = sqrt(q > 0.0 ? q : 0.0);
-  const double scale = sqrt(dmax);
-  const bool degenerate = r == 0.0 || nrm <= 1e-12 * scale || nrm == 0.0;
-  Sync()();
-  if (t < K) S.C[t] = degenerate ? invK : invK + (r / nrm) * S.a[t];  // weights
-  Sync()();
+  cagrad_primal<Sync>(S, K, r, invK, t);
 }
 
 // ---- register-only solvers for a compile-time K --------------------------

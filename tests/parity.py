@@ -144,9 +144,17 @@ def assert_out(out_gpu_store, x64, offs, w_gpu, w_ora, out_dtype, lo_hi=None, wh
     return worst
 
 
+def oracle_method(method):
+    """The oracle's (method, exact) for a library method name."""
+    if method.endswith("-exact"):
+        return method[:-len("-exact")], True
+    return method, False
+
+
 def oracle_for(wl, rows_np, offs_np, orders_np):
-    return oracle.resolve(rows_np, offs_np, wl.method, max_iter=wl.max_iter, cagrad_c=wl.cagrad_c,
-                          orders=orders_np)
+    m, exact = oracle_method(wl.method)
+    return oracle.resolve(rows_np, offs_np, m, max_iter=wl.max_iter, cagrad_c=wl.cagrad_c,
+                          orders=orders_np, exact=exact)
 
 
 def full_parity(lib, wl, grads=None, out_dtype=None):
@@ -161,11 +169,12 @@ def full_parity(lib, wl, grads=None, out_dtype=None):
     odt = wl.dtype if out_dtype is None else ("f32" if out_dtype == torch.float32 else "bf16")
     e_g = assert_gram(res["gram"], ora["gram"], wl.dtype, wl.name)
     # stage-isolated solve: the oracle solver on the GPU's own Gram
-    w_iso, a_iso = oracle.solve(res["gram"], wl.method, wl.max_iter, wl.cagrad_c, orders_np)
+    m, exact = oracle_method(wl.method)
+    w_iso, a_iso = oracle.solve(res["gram"], m, wl.max_iter, wl.cagrad_c, orders_np, exact=exact)
     e_wi = assert_weights(res["weights"], w_iso, "weights(iso)", wl.name)
     assert_weights(res["aux"], a_iso, "aux(iso)", wl.name)
     # end to end: the oracle solver on the oracle Gram
-    skip = singular_buckets(ora["gram"]) if wl.method in ("mgda", "cagrad") else None
+    skip = singular_buckets(ora["gram"]) if m in ("mgda", "cagrad") else None
     e_we = assert_weights(res["weights"], ora["weights"], "weights(e2e)", wl.name, skip=skip)
     x64 = oracle.decode_rows(rows)
     e_o = assert_out(host_out(res["out"]), x64, offs_np, res["weights"], ora["weights"], odt,
@@ -207,3 +216,32 @@ def assert_conflicts(got, want, where="", tol_cos=1e-15, tol_sum=1e-14, sign_mar
             assert np.array_equal(neg_g, neg_o), f"{where} bucket {b}: conflict signs"
             if clear.all():
                 assert pr_g[b, 2] == pr_o[b, 2], f"{where} bucket {b}: conflict count"
+
+
+def assert_exact_weights(G, w_gpu, a_gpu, w_ora, a_ora, method, where):
+    """Exact solvers: both sides solve the same small fp64 systems by
+    different factorisations (Gaussian elimination on the GPU, least squares
+    or an inverse in the oracle), so they agree to ~cond * 1e-16.  On a
+    non-singular Gram the method variable (fp64 aux) must agree to
+    1e-7 max(1, |a|) and the fp32 weights to 1e-6 max(1, |w|).  On a singular
+    one the minimiser over the simplex need not be unique: the update
+    (measured through G) must agree to 1e-6 of the gradient scale, MGDA's
+    objective to 1e-9 of it, and the GPU variable must lie on the simplex."""
+    sing = singular_buckets(G)
+    for b in range(len(G)):
+        if not sing[b]:
+            da = np.abs(a_gpu[b] - a_ora[b]) / np.maximum(1.0, np.abs(a_ora[b]))
+            dw = np.abs(w_gpu[b] - w_ora[b]) / np.maximum(1.0, np.abs(w_ora[b]))
+            assert da.max() <= 1e-7, f"{where} bucket {b}: aux off by {da.max():.2e}"
+            assert dw.max() <= 1e-6, f"{where} bucket {b}: weights off by {dw.max():.2e}"
+            continue
+        g = G[b]
+        scale = max(float(np.max(np.diag(g))), 1e-300)
+        dd = w_gpu[b] - w_ora[b]
+        upd = float(dd @ g @ dd)                  # ||d_gpu - d_ora||^2
+        assert upd <= (1e-6) ** 2 * scale * max(1.0, float(np.abs(w_ora[b]).sum()) ** 2), \
+            f"{where} bucket {b} (singular): updates differ"
+        if method == "mgda":
+            qg, qo = float(a_gpu[b] @ g @ a_gpu[b]), float(a_ora[b] @ g @ a_ora[b])
+            assert abs(qg - qo) <= 1e-9 * scale, f"{where} bucket {b} (singular): objective"
+        assert a_gpu[b].min() >= -1e-12 and abs(a_gpu[b].sum() - 1.0) <= 1e-9

@@ -122,6 +122,22 @@ def test_conflicts_argument_errors(b):
     assert L.bkmoo_conflicts(4, 3, g, None, None, None, None) == -1    # no output
 
 
+def test_exact_method_argument_errors(b):
+    L = b._lib
+    g, w = FAKE, FAKE + (1 << 20)
+    hp = b._Hparams(0, 0.5, None)
+    assert L.bkmoo_solve(11, 3, g, 4, None, w, None, None) == -2                    # K > 10
+    assert L.bkmoo_solve(11, 3, g, 5, ctypes.byref(hp), w, None, None) == -2
+    assert L.bkmoo_solve(4, 3, g, 5, None, w, None, None) == -1                     # c needed
+    bad = b._Hparams(0, 1.0, None)
+    assert L.bkmoo_solve(4, 3, g, 5, ctypes.byref(bad), w, None, None) == -1        # c out of range
+    assert L.bkmoo_solve(4, 3, g, 6, ctypes.byref(hp), w, None, None) == -1         # no such method
+    path = ctypes.c_int32(0)
+    assert L.bkmoo_resolve_path(11, 1 << 20, 2, 1, 1, 1, 4, 0, ctypes.byref(path)) == -2
+    assert L.bkmoo_resolve_path(4, 1 << 20, 2, 1, 1, 1, 4, 0, ctypes.byref(path)) == 0
+    assert path.value == b.PATH_TWO_PASS
+
+
 def test_grid_override_rejects_negative(b):
     assert b._lib.bkmoo_set_grid_override(-1) == -1
     assert b._lib.bkmoo_set_grid_override(0) == 0

@@ -10,6 +10,9 @@ At these sizes the oracle cannot redo everything, so each workload checks:
   against the exactly computed weighted sum of the GPU weights (bf16 output:
   the correctly rounded value; fp32 output: within K fp32 ulps of the sum
   of magnitudes);
+* the exact MGDA and CAGrad solvers on the GPU's Gram (K <= 10): every
+  bucket, or 48 seeded buckets when there are thousands, against the
+  oracle's exact solvers;
 * conflict diagnostics: every bucket against the oracle on the GPU's Gram,
   sampled buckets against the oracle's Gram, and, for the unit-scale
   normal workloads, every bucket's cosines against the correlation matrix
@@ -24,8 +27,8 @@ import torch
 
 import oracle
 from synth import WORKLOADS, fill_grads, host_rows
-from tests.parity import TAU, assert_conflicts, assert_gram, assert_out, assert_weights, run_resolve, \
-    singular_buckets
+from tests.parity import TAU, assert_conflicts, assert_exact_weights, assert_gram, assert_out, \
+    assert_weights, run_resolve, singular_buckets
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -47,6 +50,17 @@ def _check_workload(lib, wl, grads, offs, order):
     if wl.method in ("mgda", "cagrad"):
         a = res["aux"]
         assert a.min() >= -1e-12 and np.abs(a.sum(1) - 1).max() <= 1e-9
+    # exact solvers on the GPU Gram
+    if wl.K <= 10 and wl.method in ("mgda", "cagrad"):
+        Gd = torch.from_numpy(res["gram"]).to(grads.device)
+        W_ex, A_ex = lib.solve(Gd, f"{wl.method}-exact", cagrad_c=wl.cagrad_c)
+        W_ex, A_ex = W_ex.cpu().numpy().astype(np.float64), A_ex.cpu().numpy()
+        rs = np.random.default_rng(wl.seed + 77)
+        sel = np.arange(wl.B) if wl.B <= 700 else np.sort(rs.choice(wl.B, size=48, replace=False))
+        w_o, a_o = oracle.solve(res["gram"][sel], wl.method, cagrad_c=wl.cagrad_c, exact=True)
+        assert_exact_weights(res["gram"][sel], W_ex[sel], A_ex[sel], w_o, a_o, wl.method,
+                             f"{wl.name} {wl.method}-exact")
+        print(f"  exact {wl.method}: {len(sel)} buckets match the oracle", flush=True)
     # conflict diagnostics on the GPU Gram, every bucket
     conf = [t.cpu().numpy() for t in lib.conflicts(torch.from_numpy(res["gram"]).to(grads.device))]
     assert_conflicts(conf, oracle.conflicts(res["gram"]), f"{wl.name} conflicts(iso)")
