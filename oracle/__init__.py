@@ -18,6 +18,8 @@ Parity status of each function (what pins it is listed in its docstring):
   tiny buckets, no-conflict and K=2 closed forms)
 * cagrad_fw / cagrad_exact ............ pinned (primal feasibility, zero
   duality gap, random-direction search, c=0 reduction, descent bound)
+* slice_offsets, gram_reduce ........... pinned (partition of every bucket,
+  additivity of inner products over slices, exact on integer data)
 * conflicts ........................... pinned (cosines and conflict counts
   from the vectors, closed-form configurations, invariances)
 """
@@ -31,11 +33,13 @@ from .reference import (  # noqa: F401
     decode_rows,
     f64_to_bf16_bits,
     gram,
+    gram_reduce,
     mgda_exact,
     mgda_fw,
     pair_min_norm,
     pcgrad,
     resolve,
     round_to_dtype,
+    slice_offsets,
     solve,
 )

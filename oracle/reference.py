@@ -96,6 +96,35 @@ def gram(x: np.ndarray, offsets: np.ndarray) -> np.ndarray:
     return out
 
 
+def slice_offsets(offsets: np.ndarray, T: int) -> np.ndarray:
+    """Cut every bucket into T contiguous slices, the pieces T ranks would
+    each hold after exchanging bucket slices: slice t of bucket b is
+    [o_b + floor(t n_b / T), o_b + floor((t + 1) n_b / T)), n_b = o_{b+1} - o_b.
+    Returns the B*T+1 offsets of the slices, bucket-major (bucket b's
+    slices 0..T-1 are consecutive)."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    nb = len(offsets) - 1
+    out = np.empty(nb * T + 1, dtype=np.int64)
+    for b in range(nb):
+        n = int(offsets[b + 1] - offsets[b])
+        for t in range(T):
+            out[b * T + t] = int(offsets[b]) + (t * n) // T
+    out[nb * T] = offsets[nb]
+    return out
+
+
+def gram_reduce(partials: np.ndarray) -> np.ndarray:
+    """Sum per-slice partial Gram matrices partials[t, b] over the slices in
+    order t = 0, 1, ..., T-1: inner products add over disjoint pieces of a
+    bucket, as over the buckets of the whole vector (Eq. decomp), so the sum
+    is the bucket's Gram matrix.  partials: [T, B, K, K].  Returns [B, K, K]."""
+    partials = np.asarray(partials, dtype=np.float64)
+    acc = partials[0].copy()
+    for t in range(1, partials.shape[0]):
+        acc = acc + partials[t]
+    return acc
+
+
 # ----------------------------------------------------------------------------
 # MGDA (Eq. mgda; Eq. shard-mgda over the simplex, Appendix B)
 # ----------------------------------------------------------------------------

@@ -484,6 +484,8 @@ def check_conflicts(fn):
 
 def test_conflicts_match_vector_cosines():
     check_conflicts(oracle.conflicts)
+    check_slice_offsets(oracle.slice_offsets)
+    check_gram_reduce(oracle.gram_reduce)
 
 
 def test_conflicts_closed_forms():
@@ -526,6 +528,70 @@ def test_conflicts_non_finite_bucket():
     cos, summ, pairs = oracle.conflicts(G)
     assert np.all(np.isnan(cos[1])) and np.all(np.isnan(summ[1])) and np.all(pairs[1] == -1)
     assert tuple(pairs[0]) == (0, 1, 0)
+
+
+# ----------------------------------------------------------------------------
+# bucket slices and the slice-order Gram sum (Eq. decomp over slices)
+# ----------------------------------------------------------------------------
+
+
+def check_slice_offsets(fn):
+    rng = np.random.default_rng(23)
+    for T in (1, 2, 3, 7, 8):
+        lens = [0, 1, 2, 5, 7, 64, 1000, int(rng.integers(1, 5000))]
+        offs = np.concatenate([[0], np.cumsum(lens)])
+        so = fn(offs, T)
+        assert len(so) == len(lens) * T + 1 and so[0] == 0 and so[-1] == offs[-1]
+        assert np.all(np.diff(so) >= 0)
+        for b, n in enumerate(lens):
+            assert so[b * T] == offs[b]
+            sizes = np.diff(so[b * T:(b + 1) * T + 1])
+            assert sizes.sum() == n and sizes.max() - sizes.min() <= 1
+            # every element's slice, computed element by element: i lies in
+            # slice t iff t n / T <= i < (t + 1) n / T rounded down, i.e.
+            # t = ceil((i + 1) T / n) - 1
+            for i in range(n):
+                t = -((-(i + 1) * T) // n) - 1
+                assert so[b * T + t] <= offs[b] + i < so[b * T + t + 1], (T, b, i)
+
+
+def check_gram_reduce(fn):
+    rng = np.random.default_rng(24)
+    lens = [50, 1, 0, 33, 8]
+    offs = np.concatenate([[0], np.cumsum(lens)])
+    x = rng.integers(-8, 9, size=(4, offs[-1])).astype(np.float64)   # exact in fp64
+    for T in (1, 2, 5):
+        so = oracle.slice_offsets(offs, T)
+        sub = np.stack([x[:, so[i]:so[i + 1]] @ x[:, so[i]:so[i + 1]].T for i in range(len(so) - 1)])
+        parts = sub.reshape(len(lens), T, 4, 4).transpose(1, 0, 2, 3)   # [T, B, K, K]
+        full = np.stack([x[:, offs[b]:offs[b + 1]] @ x[:, offs[b]:offs[b + 1]].T for b in range(len(lens))])
+        assert np.array_equal(fn(parts), full)
+
+
+def test_slice_offsets_partition_every_bucket():
+    check_slice_offsets(oracle.slice_offsets)
+
+
+def test_gram_reduce_is_additive_over_slices():
+    check_gram_reduce(oracle.gram_reduce)
+    # real-valued data: equal to the whole bucket's Gram to fp64 rounding
+    rng = np.random.default_rng(25)
+    x = rng.standard_normal((3, 1000))
+    offs = np.array([0, 1000])
+    so = oracle.slice_offsets(offs, 8)
+    parts = np.stack([oracle.gram(x, so[t:t + 2] - 0) for t in range(8)])
+    np.testing.assert_allclose(oracle.gram_reduce(parts)[0], x @ x.T, rtol=1e-13, atol=1e-12)
+
+
+def test_global_moo_is_one_bucket():
+    """B = 1 (the whole vector as one bucket, global MOO): the Gram is the
+    plain matrix of inner products of the full gradients."""
+    rng = np.random.default_rng(26)
+    x = rng.standard_normal((4, 777))
+    G = oracle.gram(x, np.array([0, 777]))[0]
+    for i in range(4):
+        for j in range(4):
+            assert abs(G[i, j] - math.fsum(x[i] * x[j])) <= 1e-12
 
 
 # ----------------------------------------------------------------------------
@@ -596,6 +662,8 @@ def test_checks_pass_on_the_oracle():
     check_cagrad(oracle.cagrad_exact)
     check_combine(oracle.combine)
     check_conflicts(oracle.conflicts)
+    check_slice_offsets(oracle.slice_offsets)
+    check_gram_reduce(oracle.gram_reduce)
 
 
 def _gram_off_by_one(x, offs):
@@ -687,6 +755,23 @@ def _conflicts_mutant(**change):
     return fn
 
 
+def _slice_offsets_ceil(offs, T):
+    # mistake: rounds the slice starts up
+    out = []
+    for b in range(len(offs) - 1):
+        n = int(offs[b + 1] - offs[b])
+        out += [int(offs[b]) + -((-t * n) // T) for t in range(T)]
+    return np.array(out + [int(offs[-1])])
+
+
+def _gram_reduce_drops_last(parts):
+    # mistake: the last slice is not added
+    acc = np.array(parts[0], dtype=np.float64)
+    for t in range(1, len(parts) - 1):
+        acc = acc + parts[t]
+    return acc
+
+
 @pytest.mark.parametrize("check,mutant", [
     (check_gram, _gram_off_by_one),
     (check_mgda_k2, _fw_swapped_pair),
@@ -698,6 +783,8 @@ def _conflicts_mutant(**change):
     (check_conflicts, _conflicts_mutant(le=True)),
     (check_conflicts, _conflicts_mutant(last_tie=True)),
     (check_conflicts, _conflicts_mutant(ddof1=True)),
+    (check_slice_offsets, _slice_offsets_ceil),
+    (check_gram_reduce, _gram_reduce_drops_last),
 ])
 def test_planted_mistakes_are_caught(check, mutant):
     with pytest.raises(AssertionError):
