@@ -249,6 +249,34 @@ def main():
     extras["solve_cagrad_exact_k10_b6564"] = time_solve(G10, "cagrad-exact", reps=2)
     log("exact solvers (ms): " + ", ".join(f"{k} {v:.3f}" for k, v in extras.items() if "exact" in k))
 
+    # the sliced mode at this shape (every bucket cut into 8 slices: the
+    # Gram pass over 8*B slice offsets, then the slice-order reduction) and
+    # global MOO (one bucket for all N); both read K*s*N bytes
+    so8 = bkmoo.slice_offsets(offs, 8)
+    ws8 = torch.empty(bkmoo.workspace_size(K, N, 8 * B, wl.dtype), dtype=torch.uint8, device=dev)
+    P8 = torch.empty((B, 8, K, K), dtype=torch.float64, device=dev)
+    G8 = torch.empty((B, K, K), dtype=torch.float64, device=dev)
+    offs1 = torch.tensor([0, N], dtype=torch.int64, device=dev)
+    ws1 = torch.empty(bkmoo.workspace_size(K, N, 1, wl.dtype), dtype=torch.uint8, device=dev)
+    G1 = torch.empty((1, K, K), dtype=torch.float64, device=dev)
+
+    def sliced():
+        bkmoo.gram(grads, so8, gram_out=P8.view(8 * B, K, K), workspace=ws8)
+        bkmoo.gram_reduce(P8, bkmoo.SLICES_BUCKET_MAJOR, gram_out=G8)
+
+    for name, fn in (("gram_sliced_T8", sliced),
+                     ("gram_global_B1", lambda: bkmoo.gram(grads, offs1, gram_out=G1, workspace=ws1))):
+        fn()
+        e0.record(stream)
+        for _ in range(3):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        extras[name] = round(e0.elapsed_time(e1) / 3, 4)
+    log(f"sliced Gram (T=8) {extras['gram_sliced_T8']:.3f} ms, global Gram (B=1) "
+        f"{extras['gram_global_B1']:.3f} ms, per-bucket Gram {st.get('gram', float('nan')):.3f} ms")
+    del ws8, P8, ws1
+
     # dominant kernel: the resident kernel (reads K*s*N once, writes s*N), or
     # the longer of the two streaming passes
     if resident:

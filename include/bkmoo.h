@@ -86,6 +86,12 @@ typedef enum {
 #define BKMOO_DEVERR_OFFSETS 0x1u /* bucket offsets rejected */
 #define BKMOO_DEVERR_TIMEOUT 0x2u /* single-read resolve: a bounded wait expired (results invalid) */
 
+/* Layout of T sets of per-slice partial Gram matrices (bkmoo_gram_reduce). */
+typedef enum {
+  BKMOO_SLICES_RANK_MAJOR = 0,   /* partial[t][b][K][K]: T gathered per-rank sets */
+  BKMOO_SLICES_BUCKET_MAJOR = 1  /* partial[b][t][K][K]: bkmoo_gram over slice offsets */
+} bkmoo_slice_layout;
+
 /* How bkmoo_resolve runs the step (bkmoo_resolve_path). */
 typedef enum {
   BKMOO_PATH_TWO_PASS = 1, /* Gram pass, solve, combine pass: reads the gradients twice */
@@ -222,6 +228,43 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
                            const bkmoo_hparams *hp, void *out, bkmoo_dtype out_dt, double *gram,
                            float *weights, double *aux, void *workspace, size_t ws_bytes,
                            hipStream_t stream);
+
+/*
+ * bkmoo_slice_offsets — cut every bucket into T contiguous slices: slice t
+ * of bucket b is [o_b + floor(t n_b / T), o_b + floor((t+1) n_b / T)),
+ * n_b = o_{b+1} - o_b, the piece rank t of T would hold after the ranks
+ * exchange bucket slices.  Inner products add over disjoint pieces
+ * (Eq. decomp), so a bucket's Gram matrix is the sum of its slices'.
+ *
+ *   bucket_offsets (in)  device int64 [B+1]
+ *   slice_offsets  (out) device int64 [B*T+1], bucket-major: bucket b's
+ *                  slices 0..T-1 are entries b*T .. b*T+T; usable as the
+ *                  bucket offsets of bkmoo_gram with B*T buckets
+ *
+ * Asynchronous on `stream`; the offsets are not validated here (bkmoo_gram
+ * validates what it is given).  BKMOO_EINVAL for B < 1, T < 1, B*T beyond
+ * int32 or a null pointer.
+ */
+bkmoo_status bkmoo_slice_offsets(int32_t B, int32_t T, const int64_t *bucket_offsets,
+                                 int64_t *slice_offsets, hipStream_t stream);
+
+/*
+ * bkmoo_gram_reduce — add T sets of per-slice partial Gram matrices in
+ * slice (rank) order t = 0, 1, ..., T-1, the same order on every rank, so
+ * every rank gets the same Gram matrices bit for bit:
+ *   gram[b] = partial(0, b) + partial(1, b) + ... + partial(T-1, b)
+ *
+ *   partial (in)  device fp64, `layout`: BKMOO_SLICES_RANK_MAJOR
+ *                 [T][B][K][K] (the gathered per-rank sets) or
+ *                 BKMOO_SLICES_BUCKET_MAJOR [B][T][K][K] (bkmoo_gram over
+ *                 bkmoo_slice_offsets)
+ *   gram    (out) device fp64 [B][K][K]; must not overlap `partial`
+ *
+ * Asynchronous on `stream`.  BKMOO_EINVAL for K < 2, B < 1, T < 1, a null
+ * pointer or an unknown layout; BKMOO_EUNSUPPORTED for K > 16.
+ */
+bkmoo_status bkmoo_gram_reduce(int32_t K, int32_t B, int32_t T, const double *partial,
+                               bkmoo_slice_layout layout, double *gram, hipStream_t stream);
 
 /*
  * bkmoo_conflicts — per-bucket gradient-conflict diagnostics from Gram

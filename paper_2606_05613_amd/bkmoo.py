@@ -51,6 +51,8 @@ def _load():
         "bkmoo_resolve": [i32, vpp, ctypes.c_int, i64, i32, vp, ctypes.c_int, ctypes.POINTER(_Hparams),
                           vp, ctypes.c_int, vp, vp, vp, vp, sz, vp],
         "bkmoo_conflicts": [i32, i32, vp, vp, vp, vp, vp],
+        "bkmoo_slice_offsets": [i32, i32, vp, vp, vp],
+        "bkmoo_gram_reduce": [i32, i32, i32, vp, ctypes.c_int, vp, vp],
         "bkmoo_read_device_error": [vp, ctypes.POINTER(u32), vp],
         "bkmoo_set_grid_override": [i32],
         "bkmoo_resolve_path": [i32, i64, i32, ctypes.c_int, ctypes.c_int, i32, ctypes.c_int, i32,
@@ -69,7 +71,7 @@ def _load():
 _lib = _load()
 
 EXPORTS = ("bkmoo_workspace_size", "bkmoo_gram", "bkmoo_solve", "bkmoo_combine", "bkmoo_resolve",
-           "bkmoo_conflicts", "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
+           "bkmoo_conflicts", "bkmoo_slice_offsets", "bkmoo_gram_reduce", "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
            "bkmoo_set_resolve_path", "bkmoo_set_wait_limit", "bkmoo_status_string")
 
 
@@ -189,6 +191,39 @@ def solve(gram_in: torch.Tensor, method: str, max_iter: int = 20, cagrad_c: floa
     _check(_lib.bkmoo_solve(K, B, gram_in.data_ptr(), METHODS[method], ctypes.byref(hp),
                             weights.data_ptr(), aux.data_ptr(), _stream_ptr(dev)), "bkmoo_solve")
     return weights, aux
+
+
+SLICES_RANK_MAJOR, SLICES_BUCKET_MAJOR = 0, 1
+
+
+def slice_offsets(bucket_offsets: torch.Tensor, T: int) -> torch.Tensor:
+    """Offsets (int64 [B*T+1], bucket-major) of T contiguous slices of every
+    bucket: slice t of bucket b starts at o_b + floor(t n_b / T)."""
+    offs = bucket_offsets
+    if offs.dtype != torch.int64 or offs.dim() != 1 or not offs.is_contiguous() or offs.device.type != "cuda":
+        raise ValueError("bucket_offsets must be a contiguous int64 GPU tensor")
+    B = offs.numel() - 1
+    out = torch.empty(B * T + 1, dtype=torch.int64, device=offs.device)
+    _check(_lib.bkmoo_slice_offsets(B, int(T), offs.data_ptr(), out.data_ptr(), _stream_ptr(offs.device)),
+           "bkmoo_slice_offsets")
+    return out
+
+
+def gram_reduce(partial: torch.Tensor, layout: int = SLICES_RANK_MAJOR,
+                gram_out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Sum per-slice partial Grams in slice order: partial fp64 [T, B, K, K]
+    (rank-major) or [B, T, K, K] (bucket-major) -> [B, K, K]."""
+    if partial.dtype != torch.float64 or partial.dim() != 4 or not partial.is_contiguous():
+        raise ValueError("partial must be a contiguous fp64 4-d tensor")
+    if layout == SLICES_RANK_MAJOR:
+        T, B, K, _ = partial.shape
+    else:
+        B, T, K, _ = partial.shape
+    if gram_out is None:
+        gram_out = torch.empty((B, K, K), dtype=torch.float64, device=partial.device)
+    _check(_lib.bkmoo_gram_reduce(K, B, T, partial.data_ptr(), int(layout), gram_out.data_ptr(),
+                                  _stream_ptr(partial.device)), "bkmoo_gram_reduce")
+    return gram_out
 
 
 def conflicts(gram_in: torch.Tensor, cosines: bool = True, summary: bool = True,

@@ -272,6 +272,27 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   return hip_status(launch_combine(a, W, out, (int)out_dt, stream));
 }
 
+bkmoo_status bkmoo_slice_offsets(int32_t B, int32_t T, const int64_t *bucket_offsets,
+                                 int64_t *slice_offsets, hipStream_t stream) {
+  if (B < 1 || T < 1 || (int64_t)B * T > INT32_MAX) return BKMOO_EINVAL;
+  if (!bucket_offsets || !slice_offsets) return BKMOO_EINVAL;
+  return hip_status(launch_slice_offsets(bucket_offsets, B, T, slice_offsets, stream));
+}
+
+bkmoo_status bkmoo_gram_reduce(int32_t K, int32_t B, int32_t T, const double *partial,
+                               bkmoo_slice_layout layout, double *gram, hipStream_t stream) {
+  if (K < kMinK || B < 1 || T < 1) return BKMOO_EINVAL;
+  if (K > kMaxK) return BKMOO_EUNSUPPORTED;
+  if (!partial || !gram) return BKMOO_EINVAL;
+  if (layout != BKMOO_SLICES_RANK_MAJOR && layout != BKMOO_SLICES_BUCKET_MAJOR) return BKMOO_EINVAL;
+  const size_t in_bytes = sizeof(double) * (size_t)T * B * K * K;
+  const size_t out_bytes = sizeof(double) * (size_t)B * K * K;
+  const char *pi = reinterpret_cast<const char *>(partial), *po = reinterpret_cast<const char *>(gram);
+  if (po < pi + in_bytes && pi < po + out_bytes) return BKMOO_EINVAL;
+  return hip_status(launch_gram_reduce(K, B, T, partial, layout == BKMOO_SLICES_BUCKET_MAJOR ? 1 : 0,
+                                       gram, stream));
+}
+
 bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *cosines,
                              double *summary, int32_t *pairs, hipStream_t stream) {
   if (K < kMinK || B < 1) return BKMOO_EINVAL;

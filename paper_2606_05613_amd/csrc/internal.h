@@ -122,6 +122,10 @@ hipError_t launch_combine(const StreamArgs &a, const float *weights, void *out, 
                           hipStream_t s);
 hipError_t launch_conflicts(int K, int B, const double *gram, double *cosines, double *summary,
                             int32_t *pairs, hipStream_t s);
+// Bucket slices and the slice-order sum of partial Grams.
+hipError_t launch_slice_offsets(const int64_t *offsets, int B, int T, int64_t *out, hipStream_t s);
+hipError_t launch_gram_reduce(int K, int B, int T, const double *partial, int bucket_major, double *gram,
+                              hipStream_t s);
 // Exact MGDA / CAGrad solvers by support enumeration (K <= kExactMaxK).
 hipError_t launch_exact_solve(int K, int B, const double *gram, int method, double c, float *weights,
                               double *aux, hipStream_t s);

@@ -138,6 +138,23 @@ def test_exact_method_argument_errors(b):
     assert path.value == b.PATH_TWO_PASS
 
 
+def test_slice_argument_errors(b):
+    L = b._lib
+    o, so = FAKE, FAKE + (1 << 20)
+    assert L.bkmoo_slice_offsets(0, 4, o, so, None) == -1
+    assert L.bkmoo_slice_offsets(3, 0, o, so, None) == -1
+    assert L.bkmoo_slice_offsets(1 << 20, 1 << 12, o, so, None) == -1    # B*T beyond int32
+    assert L.bkmoo_slice_offsets(3, 4, None, so, None) == -1
+    assert L.bkmoo_slice_offsets(3, 4, o, None, None) == -1
+    p, g = FAKE, FAKE + (64 << 20)
+    assert L.bkmoo_gram_reduce(1, 3, 2, p, 0, g, None) == -1
+    assert L.bkmoo_gram_reduce(17, 3, 2, p, 0, g, None) == -2
+    assert L.bkmoo_gram_reduce(4, 3, 0, p, 0, g, None) == -1
+    assert L.bkmoo_gram_reduce(4, 3, 2, p, 2, g, None) == -1              # layout
+    assert L.bkmoo_gram_reduce(4, 3, 2, p, 0, p + 64, None) == -1         # overlap
+    assert L.bkmoo_gram_reduce(4, 3, 2, None, 0, g, None) == -1
+
+
 def test_grid_override_rejects_negative(b):
     assert b._lib.bkmoo_set_grid_override(-1) == -1
     assert b._lib.bkmoo_set_grid_override(0) == 0

@@ -13,6 +13,10 @@ At these sizes the oracle cannot redo everything, so each workload checks:
 * the exact MGDA and CAGrad solvers on the GPU's Gram (K <= 10): every
   bucket, or 48 seeded buckets when there are thousands, against the
   oracle's exact solvers;
+* the sliced mode (8 slices per bucket, Gram pass over the slice offsets,
+  slice-order reduction) and B = 1 (one bucket for all N, global MOO)
+  against the per-bucket Grams: each Gram carries at most tau sqrt(G_ii G_jj)
+  of fp32-accumulation error, so they agree within twice that;
 * conflict diagnostics: every bucket against the oracle on the GPU's Gram,
   sampled buckets against the oracle's Gram, and, for the unit-scale
   normal workloads, every bucket's cosines against the correlation matrix
@@ -50,6 +54,19 @@ def _check_workload(lib, wl, grads, offs, order):
     if wl.method in ("mgda", "cagrad"):
         a = res["aux"]
         assert a.min() >= -1e-12 and np.abs(a.sum(1) - 1).max() <= 1e-9
+    # sliced mode and global MOO at full size
+    tau = TAU[wl.dtype]
+    so = lib.slice_offsets(offs, 8)
+    G8 = lib.gram_reduce(lib.gram(grads, so).view(wl.B, 8, wl.K, wl.K), lib.SLICES_BUCKET_MAJOR)
+    G8 = G8.cpu().numpy()
+    d = np.sqrt(np.einsum("bii->bi", np.maximum(res["gram"], 0)))
+    assert np.all(np.abs(G8 - res["gram"]) <= 2 * tau * d[:, :, None] * d[:, None, :] + 1e-300), \
+        f"{wl.name}: sliced Grams"
+    G1 = lib.gram(grads, torch.tensor([0, wl.N], dtype=torch.int64, device=grads.device)).cpu().numpy()[0]
+    Gs = res["gram"].sum(0)
+    dg = np.sqrt(np.maximum(np.diag(Gs), 0))
+    assert np.all(np.abs(G1 - Gs) <= 2 * tau * np.outer(dg, dg)), f"{wl.name}: global Gram"
+    print("  sliced (T=8) and global (B=1) Grams agree", flush=True)
     # exact solvers on the GPU Gram
     if wl.K <= 10 and wl.method in ("mgda", "cagrad"):
         Gd = torch.from_numpy(res["gram"]).to(grads.device)
