@@ -5,12 +5,13 @@
 // cagrad through its dual), both from the bucket's Gram matrix alone.
 //
 // One wavefront per bucket, fp64, K <= 10.  The 2^K - 1 supports S are
-// spread over the 64 lanes.  Each lane writes its support's small linear
-// system into LDS (the 64 lanes' copies interleaved, so one access of the
-// wavefront touches 64 consecutive words) and solves it by Gaussian
-// elimination with partial pivoting; a support whose system has an exactly
-// zero pivot is skipped.  Candidates are ranked in the order "by support
-// size, then lexicographically", which fixes every tie-break:
+// ranked in the order "by support size, then lexicographically", which fixes
+// every tie-break, and dealt to the 64 lanes in rank order, so the lanes of
+// a wavefront mostly hold supports of one size.  Each lane builds its
+// support's small linear system in registers (a solver instantiated per
+// support size, fully unrolled, row exchanges done by selects so every index
+// is static) and solves it by Gaussian elimination with partial pivoting; a
+// support whose system has an exactly zero pivot is skipped:
 //
 // MGDA.  On S the stationarity conditions G_SS a_S = mu 1, 1^T a_S = 1 form
 // a bordered (|S|+1)-square system (non-singular exactly when the g_t, t in
@@ -42,140 +43,164 @@ __device__ __forceinline__ int binom(int n, int k) {
   return r;
 }
 
-// Position of support `m` (bit t = task t) among the non-empty subsets of
+// The support of rank r (bit t = task t) among the non-empty subsets of
 // {0..K-1} ordered by size, then lexicographically.
-__device__ int support_rank(uint32_t m, int K) {
-  const int s = __builtin_popcount(m);
-  int r = 0;
-  for (int t = 1; t < s; ++t) r += binom(K, t);
-  int prev = -1, i = 0;
-  for (int c = 0; c < K; ++c)
-    if ((m >> c) & 1u) {
-      ++i;
-      for (int j = prev + 1; j < c; ++j) r += binom(K - 1 - j, s - i);
-      prev = c;
-    }
-  return r;
-}
-
-// This lane's matrix, rows of `stride` entries: entry (r, c) at
-// M[(r * stride + c) * kWave].
-struct LaneMat {
-  double *M;
-  int stride;
-  __device__ __forceinline__ double &operator()(int r, int c) const {
-    return M[(r * stride + c) * kWave];
+__device__ uint32_t support_of_rank(int r, int K) {
+  int s = 1, base = 0;
+  while (r >= base + binom(K, s)) {
+    base += binom(K, s);
+    ++s;
   }
-};
+  int rr = r - base, c = 0;
+  uint32_t m = 0;
+  for (int i = 1; i <= s; ++i) {
+    while (binom(K - 1 - c, s - i) <= rr) {
+      rr -= binom(K - 1 - c, s - i);
+      ++c;
+    }
+    m |= 1u << c;
+    ++c;
+  }
+  return m;
+}
 
 // Gaussian elimination with partial pivoting (the first entry of largest
-// magnitude) on an n x ncols augmented matrix (ncols - n right-hand sides).
-// False if a pivot is exactly zero; otherwise the solutions overwrite
-// columns n .. ncols - 1.
-__device__ bool lane_solve(const LaneMat &A, int n, int ncols) {
-  for (int k = 0; k < n; ++k) {
+// magnitude) on the N x (N + M) augmented matrix A, fully unrolled.  False if
+// a pivot is exactly zero; otherwise the solutions overwrite columns N..N+M-1.
+template <int N, int M>
+__device__ __forceinline__ bool ge_solve(double (&A)[N][N + M]) {
+  bool ok = true;
+#pragma unroll
+  for (int k = 0; k < N; ++k) {
+    double pv = fabs(A[k][k]);
     int p = k;
-    double pv = fabs(A(k, k));
-    for (int r = k + 1; r < n; ++r) {
-      const double v = fabs(A(r, k));
-      if (v > pv) {
-        pv = v;
-        p = r;
+#pragma unroll
+    for (int r = k + 1; r < N; ++r) {
+      const double v = fabs(A[r][k]);
+      const bool gt = v > pv;
+      pv = gt ? v : pv;
+      p = gt ? r : p;
+    }
+    ok = ok && pv != 0.0;
+#pragma unroll
+    for (int r = k + 1; r < N; ++r) {
+      const bool sw = p == r;
+#pragma unroll
+      for (int c = k; c < N + M; ++c) {
+        const double x = A[k][c], y = A[r][c];
+        A[k][c] = sw ? y : x;
+        A[r][c] = sw ? x : y;
       }
     }
-    if (pv == 0.0) return false;
-    if (p != k)
-      for (int c = k; c < ncols; ++c) {
-        const double tmp = A(k, c);
-        A(k, c) = A(p, c);
-        A(p, c) = tmp;
-      }
-    const double piv = A(k, k);
-    for (int r = k + 1; r < n; ++r) {
-      const double f = A(r, k) / piv;
-      for (int c = k + 1; c < ncols; ++c) A(r, c) -= f * A(k, c);
-      A(r, k) = 0.0;
+    const double piv = pv != 0.0 ? A[k][k] : 1.0;
+#pragma unroll
+    for (int r = k + 1; r < N; ++r) {
+      const double f = A[r][k] / piv;
+#pragma unroll
+      for (int c = k + 1; c < N + M; ++c) A[r][c] -= f * A[k][c];
+      A[r][k] = 0.0;
     }
   }
-  for (int j = n; j < ncols; ++j)
-    for (int r = n - 1; r >= 0; --r) {
-      double s = A(r, j);
-      for (int c = r + 1; c < n; ++c) s -= A(r, c) * A(c, j);
-      A(r, j) = s / A(r, r);
+#pragma unroll
+  for (int j = N; j < N + M; ++j)
+#pragma unroll
+    for (int r = N - 1; r >= 0; --r) {
+      double s = A[r][j];
+#pragma unroll
+      for (int c = r + 1; c < N; ++c) s -= A[r][c] * A[c][j];
+      A[r][j] = s / (A[r][r] != 0.0 ? A[r][r] : 1.0);
     }
-  return true;
+  return ok;
 }
 
-// MGDA on support m of the normalised Gram Gn: solves the bordered system
-// and runs the feasibility and minimum-norm checks.  On success the support's
-// simplex weights (clipped, renormalised) are in column |S|+1 of rows
-// 0..|S|-1, in increasing task order, and *q = a^T Gn a.
-__device__ bool mgda_support(const double *Gn, int K, uint32_t m, const LaneMat &A, double *q) {
-  int idx[kExactMaxK];
-  int s = 0;
-  for (int t = 0; t < K; ++t)
-    if ((m >> t) & 1u) idx[s++] = t;
-  const int n = s + 1, sol = s + 1;
-  for (int u = 0; u < s; ++u) {
-    for (int v = 0; v < s; ++v) A(u, v) = Gn[idx[u] * K + idx[v]];
-    A(u, s) = 1.0;
-    A(u, sol) = 0.0;
+// Tasks of support m in increasing order.
+template <int S>
+__device__ __forceinline__ void support_tasks(uint32_t m, int (&idx)[S]) {
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+    idx[u] = __builtin_ctz(m);
+    m &= m - 1u;
   }
-  for (int v = 0; v < s; ++v) A(s, v) = 1.0;
-  A(s, s) = 0.0;
-  A(s, sol) = 1.0;
-  if (!lane_solve(A, n, s + 2)) return false;
-  double amin = s < K ? 0.0 : A(0, sol), sum = 0.0;
-  for (int u = 0; u < s; ++u) {
-    const double a = A(u, sol);
-    amin = a < amin ? a : amin;
-    sum += a;
+}
+
+// MGDA on a support of S tasks of the normalised Gram Gn: solves the
+// bordered system and runs the feasibility and minimum-norm checks.  On
+// success a[0..S) holds the clipped, renormalised weights of the support's
+// tasks in increasing task order and *q = a^T Gn a.
+template <int S>
+__device__ bool mgda_support(const double *Gn, int K, uint32_t m, double (&a)[S], double *q) {
+  int idx[S];
+  support_tasks<S>(m, idx);
+  double A[S + 1][S + 2];
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+#pragma unroll
+    for (int v = 0; v < S; ++v) A[u][v] = Gn[idx[u] * K + idx[v]];
+    A[u][S] = 1.0;
+    A[u][S + 1] = 0.0;
+  }
+#pragma unroll
+  for (int v = 0; v < S; ++v) A[S][v] = 1.0;
+  A[S][S] = 0.0;
+  A[S][S + 1] = 1.0;
+  if (!ge_solve<S + 1, 1>(A)) return false;
+  double amin = S < K ? 0.0 : A[0][S + 1], sum = 0.0;
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+    amin = A[u][S + 1] < amin ? A[u][S + 1] : amin;
+    sum += A[u][S + 1];
   }
   if (!(amin >= -1e-10) || !(fabs(sum - 1.0) <= 1e-9)) return false;
   double csum = 0.0;
-  for (int u = 0; u < s; ++u) {
-    const double a = A(u, sol) > 0.0 ? A(u, sol) : 0.0;
-    A(u, sol) = a;
-    csum += a;
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+    a[u] = A[u][S + 1] > 0.0 ? A[u][S + 1] : 0.0;
+    csum += a[u];
   }
-  for (int u = 0; u < s; ++u) A(u, sol) = A(u, sol) / csum;
+#pragma unroll
+  for (int u = 0; u < S; ++u) a[u] = a[u] / csum;
   // (Gn a)_t over every task, a^T Gn a, and the minimum-norm check
   double qq = 0.0;
-  for (int u = 0; u < s; ++u) {
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
     double g = 0.0;
-    for (int v = 0; v < s; ++v) g += Gn[idx[u] * K + idx[v]] * A(v, sol);
-    qq += A(u, sol) * g;
+#pragma unroll
+    for (int v = 0; v < S; ++v) g += Gn[idx[u] * K + idx[v]] * a[v];
+    qq += a[u] * g;
   }
   for (int t = 0; t < K; ++t) {
     double g = 0.0;
-    for (int v = 0; v < s; ++v) g += Gn[t * K + idx[v]] * A(v, sol);
+#pragma unroll
+    for (int v = 0; v < S; ++v) g += Gn[t * K + idx[v]] * a[v];
     if (!(g >= qq - 1e-9)) return false;
   }
   *q = qq;
   return true;
 }
 
-// CAGrad candidate `root` (0: smaller lam, 1: larger) on support m (|m| >= 2):
-// on success the simplex point w_S is in column |S| of rows 0..|S|-1 and *F is
-// its dual objective.
+// CAGrad candidate `root` (0: smaller lam, 1: larger) on a support of S >= 2
+// tasks: on success w[0..S) holds the simplex point on the support's tasks
+// and *F its dual objective.
+template <int S>
 __device__ bool cagrad_support(const double *G, const double *bvec, double r, int K, uint32_t m,
-                               int root, const LaneMat &A, double *F) {
-  int idx[kExactMaxK];
-  int s = 0;
-  for (int t = 0; t < K; ++t)
-    if ((m >> t) & 1u) idx[s++] = t;
-  const int c1 = s, cb = s + 1;  // columns of H 1 and H b_S
-  for (int u = 0; u < s; ++u) {
-    for (int v = 0; v < s; ++v) A(u, v) = G[idx[u] * K + idx[v]];
-    A(u, c1) = 1.0;
-    A(u, cb) = bvec[idx[u]];
+                               int root, double (&w)[S], double *F) {
+  int idx[S];
+  support_tasks<S>(m, idx);
+  double A[S][S + 2];  // [G_SS | 1 | b_S]
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+#pragma unroll
+    for (int v = 0; v < S; ++v) A[u][v] = G[idx[u] * K + idx[v]];
+    A[u][S] = 1.0;
+    A[u][S + 1] = bvec[idx[u]];
   }
-  if (!lane_solve(A, s, s + 2)) return false;
+  if (!ge_solve<S, 2>(A)) return false;
   double qa = 0.0, h1b = 0.0, hbb = 0.0;
-  for (int u = 0; u < s; ++u) {
-    qa += A(u, c1);
-    h1b += A(u, c1) * bvec[idx[u]];
-    hbb += bvec[idx[u]] * A(u, cb);
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+    qa += A[u][S];
+    h1b += A[u][S] * bvec[idx[u]];
+    hbb += bvec[idx[u]] * A[u][S + 1];
   }
   const double qb = -2.0 * h1b, qc = hbb - r * r;
   const double disc = qb * qb - 4.0 * qa * qc;
@@ -183,26 +208,30 @@ __device__ bool cagrad_support(const double *G, const double *bvec, double r, in
   const double sq = sqrt(disc);
   const double lam = root == 0 ? (-qb - sq) / (2.0 * qa) : (-qb + sq) / (2.0 * qa);
   double vmin = 0.0, vsum = 0.0;
-  for (int u = 0; u < s; ++u) {
-    const double v = (lam * A(u, c1) - A(u, cb)) / r;
-    A(u, c1) = v;  // v_S, then w_S, in column |S|
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+    const double v = (lam * A[u][S] - A[u][S + 1]) / r;
+    w[u] = v;
     vmin = u == 0 || v < vmin ? v : vmin;
     vsum += v;
   }
   if (!(vmin >= -1e-12) || !(vsum > 0.0)) return false;
   double csum = 0.0;
-  for (int u = 0; u < s; ++u) {
-    const double w = A(u, c1) > 0.0 ? A(u, c1) : 0.0;
-    A(u, c1) = w;
-    csum += w;
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+    w[u] = w[u] > 0.0 ? w[u] : 0.0;
+    csum += w[u];
   }
   double bw = 0.0, q = 0.0;
-  for (int u = 0; u < s; ++u) A(u, c1) = A(u, c1) / csum;
-  for (int u = 0; u < s; ++u) {
-    bw += bvec[idx[u]] * A(u, c1);
+#pragma unroll
+  for (int u = 0; u < S; ++u) w[u] = w[u] / csum;
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+    bw += bvec[idx[u]] * w[u];
     double g = 0.0;
-    for (int v = 0; v < s; ++v) g += A(v, c1) * G[idx[v] * K + idx[u]];
-    q += g * A(u, c1);
+#pragma unroll
+    for (int v = 0; v < S; ++v) g += w[v] * G[idx[v] * K + idx[u]];
+    q += g * w[u];
   }
   const double f = bw + r * sqrt(q > 0.0 ? q : 0.0);
   if (!__builtin_isfinite(f)) return false;
@@ -210,26 +239,71 @@ __device__ bool cagrad_support(const double *G, const double *bvec, double r, in
   return true;
 }
 
+// Size dispatch: run the support-size instantiation for |m| and, if `dst`
+// is given, scatter its point onto the K tasks.
+__device__ bool mgda_any(const double *Gn, int K, uint32_t m, double *q, double *dst) {
+  switch (__builtin_popcount(m)) {
+#define BKMOO_MGDA_CASE(n)                                                 \
+  case n: {                                                                \
+    double a[n];                                                           \
+    if (!mgda_support<n>(Gn, K, m, a, q)) return false;                    \
+    if (dst) {                                                             \
+      int idx[n];                                                          \
+      support_tasks<n>(m, idx);                                            \
+      for (int i = 0; i < K; ++i) dst[i] = 0.0;                            \
+      _Pragma("unroll") for (int u = 0; u < n; ++u) dst[idx[u]] = a[u];    \
+    }                                                                      \
+    return true;                                                           \
+  }
+    BKMOO_MGDA_CASE(1) BKMOO_MGDA_CASE(2) BKMOO_MGDA_CASE(3) BKMOO_MGDA_CASE(4) BKMOO_MGDA_CASE(5)
+    BKMOO_MGDA_CASE(6) BKMOO_MGDA_CASE(7) BKMOO_MGDA_CASE(8) BKMOO_MGDA_CASE(9) BKMOO_MGDA_CASE(10)
+#undef BKMOO_MGDA_CASE
+    default: return false;
+  }
+}
+
+__device__ bool cagrad_any(const double *G, const double *bvec, double r, int K, uint32_t m, int root,
+                           double *F, double *dst) {
+  switch (__builtin_popcount(m)) {
+#define BKMOO_CAGRAD_CASE(n)                                                   \
+  case n: {                                                                    \
+    double w[n];                                                               \
+    if (!cagrad_support<n>(G, bvec, r, K, m, root, w, F)) return false;        \
+    if (dst) {                                                                 \
+      int idx[n];                                                              \
+      support_tasks<n>(m, idx);                                                \
+      for (int i = 0; i < K; ++i) dst[i] = 0.0;                                \
+      _Pragma("unroll") for (int u = 0; u < n; ++u) dst[idx[u]] = w[u];        \
+    }                                                                          \
+    return true;                                                               \
+  }
+    BKMOO_CAGRAD_CASE(2) BKMOO_CAGRAD_CASE(3) BKMOO_CAGRAD_CASE(4) BKMOO_CAGRAD_CASE(5)
+    BKMOO_CAGRAD_CASE(6) BKMOO_CAGRAD_CASE(7) BKMOO_CAGRAD_CASE(8) BKMOO_CAGRAD_CASE(9)
+    BKMOO_CAGRAD_CASE(10)
+#undef BKMOO_CAGRAD_CASE
+    default: return false;
+  }
+}
+
 // (F, slot) is lexicographically smaller than (G, other).
 __device__ __forceinline__ bool before(double f, int slot, double g, int other) {
   return f < g || (f == g && slot < other);
 }
 
-template <int K>
-__global__ __launch_bounds__(kWave) void exact_solve_kernel(const double *__restrict__ gram, int method,
-                                                            double c, float *__restrict__ weights,
+constexpr int kMaxSupports = (1 << kExactMaxK) - 1;
+
+__global__ __launch_bounds__(kWave) void exact_solve_kernel(int K, const double *__restrict__ gram,
+                                                            int method, double c,
+                                                            float *__restrict__ weights,
                                                             double *__restrict__ aux) {
-  constexpr int NSUB = (1 << K) - 1;
-  constexpr int COLS = K + 2;
   __shared__ Shared S;
-  __shared__ double mats[(K + 1) * COLS * kWave];
-  __shared__ double Gn[K * K];
-  __shared__ double qv[NSUB];
-  __shared__ uint32_t ok[NSUB];  // mask | kept << 16
+  __shared__ double Gn[kExactMaxK * kExactMaxK];
+  __shared__ double qv[kMaxSupports];
+  __shared__ uint32_t ok[kMaxSupports];  // mask | kept << 16
   __shared__ int choice;
   const int64_t b = blockIdx.x;
   const int t = threadIdx.x;
-  const LaneMat A{mats + t, COLS};
+  const int nsub = (1 << K) - 1;
   solver_load_gram<WaveSync>(S, K, gram + b * K * K, t, kWave);
   if (S.bad) {
     if (t < K) {
@@ -245,10 +319,10 @@ __global__ __launch_bounds__(kWave) void exact_solve_kernel(const double *__rest
     const double scale = dmax > 1e-300 ? dmax : 1e-300;
     for (int i = t; i < K * K; i += kWave) Gn[i] = S.G[i] / scale;
     WaveSync()();
-    for (uint32_t m = t + 1; m <= (uint32_t)NSUB; m += kWave) {
+    for (int rk = t; rk < nsub; rk += kWave) {
+      const uint32_t m = support_of_rank(rk, K);
       double q = 0.0;
-      const bool kept = mgda_support(Gn, K, m, A, &q);
-      const int rk = support_rank(m, K);
+      const bool kept = mgda_any(Gn, K, m, &q, nullptr);
       qv[rk] = q;
       ok[rk] = m | (kept ? 1u << 16 : 0u);
     }
@@ -256,19 +330,15 @@ __global__ __launch_bounds__(kWave) void exact_solve_kernel(const double *__rest
     if (t == 0) {
       int best = -1;
       double bq = 0.0;
-      for (int rk = 0; rk < NSUB; ++rk)
+      for (int rk = 0; rk < nsub; ++rk)
         if ((ok[rk] >> 16) && (best < 0 || qv[rk] < bq - 1e-12)) {
           best = rk;
           bq = qv[rk];
         }
       choice = best;
       if (best >= 0) {
-        const uint32_t m = ok[best] & 0xFFFFu;
         double q;
-        mgda_support(Gn, K, m, A, &q);
-        const int s = __builtin_popcount(m);
-        int u = 0;
-        for (int i = 0; i < K; ++i) S.a[i] = ((m >> i) & 1u) ? A(u++, s + 1) : 0.0;
+        mgda_any(Gn, K, ok[best] & 0xFFFFu, &q, S.a);
       }
     }
     WaveSync()();
@@ -298,12 +368,11 @@ __global__ __launch_bounds__(kWave) void exact_solve_kernel(const double *__rest
       bslot = t;
     }
     if (r > 0.0)
-      for (uint32_t m = t + 1; m <= (uint32_t)NSUB; m += kWave) {
-        if (__builtin_popcount(m) < 2) continue;
-        const int rk = support_rank(m, K);
+      for (int rk = K + t; rk < nsub; rk += kWave) {
+        const uint32_t m = support_of_rank(rk, K);
         for (int root = 0; root < 2; ++root) {
           double f;
-          if (cagrad_support(S.G, S.bvec, r, K, m, root, A, &f)) {
+          if (cagrad_any(S.G, S.bvec, r, K, m, root, &f, nullptr)) {
             const int slot = K + 2 * (rk - K) + root;
             if (before(f, slot, bf, bslot)) {
               bf = f;
@@ -328,13 +397,8 @@ __global__ __launch_bounds__(kWave) void exact_solve_kernel(const double *__rest
       if (bslot < K) {
         for (int i = 0; i < K; ++i) S.a[i] = i == bslot ? 1.0 : 0.0;
       } else {
-        const int root = (bslot - K) & 1;
-        const uint32_t m = bmask;
         double f;
-        cagrad_support(S.G, S.bvec, r, K, m, root, A, &f);
-        const int s = __builtin_popcount(m);
-        int u = 0;
-        for (int i = 0; i < K; ++i) S.a[i] = ((m >> i) & 1u) ? A(u++, s) : 0.0;
+        cagrad_any(S.G, S.bvec, r, K, bmask, (bslot - K) & 1, &f, S.a);
       }
     }
     WaveSync()();
@@ -350,29 +414,13 @@ __global__ __launch_bounds__(kWave) void exact_solve_kernel(const double *__rest
   }
 }
 
-template <int K>
-void launch_exact_t(int B, const double *gram, int method, double c, float *weights, double *aux,
-                    hipStream_t s) {
-  hipLaunchKernelGGL(exact_solve_kernel<K>, dim3((unsigned)B), dim3(kWave), 0, s, gram, method, c,
-                     weights, aux);
-}
-
 }  // namespace
 
 hipError_t launch_exact_solve(int K, int B, const double *gram, int method, double c, float *weights,
                               double *aux, hipStream_t s) {
-  switch (K) {
-    case 2: launch_exact_t<2>(B, gram, method, c, weights, aux, s); break;
-    case 3: launch_exact_t<3>(B, gram, method, c, weights, aux, s); break;
-    case 4: launch_exact_t<4>(B, gram, method, c, weights, aux, s); break;
-    case 5: launch_exact_t<5>(B, gram, method, c, weights, aux, s); break;
-    case 6: launch_exact_t<6>(B, gram, method, c, weights, aux, s); break;
-    case 7: launch_exact_t<7>(B, gram, method, c, weights, aux, s); break;
-    case 8: launch_exact_t<8>(B, gram, method, c, weights, aux, s); break;
-    case 9: launch_exact_t<9>(B, gram, method, c, weights, aux, s); break;
-    case 10: launch_exact_t<10>(B, gram, method, c, weights, aux, s); break;
-    default: return hipErrorInvalidValue;
-  }
+  if (K < kMinK || K > kExactMaxK) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(exact_solve_kernel, dim3((unsigned)B), dim3(kWave), 0, s, K, gram, method, c, weights,
+                     aux);
   return hipGetLastError();
 }
 
