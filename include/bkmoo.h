@@ -217,10 +217,12 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  *             fixed, grid-independent) order, so results agree with the
  *             two-pass path to rounding, not bitwise.  A bucket larger than
  *             the chip holds is read twice, still correct.
- * The resident path is chosen when the average bucket holds at least
- * 32 MiB of gradients, fits on chip, and the solve is short (PCGrad, mean,
- * or at most 2 Frank-Wolfe iterations): each bucket's solve lies on the
- * resident kernel's critical path.  bkmoo_resolve_path reports the choice;
+ * The resident path is chosen when the call has at least 32 buckets, the
+ * average bucket holds at least 32 MiB of gradients and fits on chip, and
+ * the solve is short (PCGrad, mean, or at most 2 Frank-Wolfe iterations):
+ * each bucket's solve lies on the resident kernel's critical path, and the
+ * cooperative launch costs more per call than the streaming passes, which
+ * stay faster up to about 16-24 buckets.  bkmoo_resolve_path reports the choice;
  * bkmoo_set_resolve_path forces one.
  */
 bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,

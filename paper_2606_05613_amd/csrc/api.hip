@@ -20,9 +20,14 @@ std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the resident path's b
 // solve is short: the solve of each bucket sits on the kernel's critical
 // path (a 20-iteration Frank-Wolfe costs about 7 us per bucket there, more
 // than the second read it saves on 25 MiB buckets), so iterative solvers
-// stay on the two-pass path unless they run at most kResidentMaxIters.
+// stay on the two-pass path unless they run at most kResidentMaxIters.  The
+// cooperative kernel also costs a few tens of microseconds per call more
+// than the streaming passes (measured on 25 MiB K=4 buckets: two-pass ahead
+// up to 8 buckets per call, resident ahead from about 16 (mean) or 24
+// (PCGrad)), so small calls stay on the two-pass path too.
 constexpr double kResidentMinBucketBytes = 32.0 * (1 << 20);
 constexpr int kResidentMaxIters = 2;
+constexpr int kResidentMinBuckets = 32;
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cu_count[kMaxDevices];
@@ -131,7 +136,10 @@ int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int m
   const double bucket_bytes = avg_elems * K * elem_bytes(dt);
   const double fits = (double)resident_segment_elems(K, dt) * g;
   const bool cheap_solve = method == BKMOO_PCGRAD || method == BKMOO_MEAN || iters <= kResidentMaxIters;
-  return bucket_bytes >= kResidentMinBucketBytes && avg_elems <= fits && cheap_solve ? g : 0;
+  return B >= kResidentMinBuckets && bucket_bytes >= kResidentMinBucketBytes && avg_elems <= fits &&
+                 cheap_solve
+             ? g
+             : 0;
 }
 
 }  // namespace
