@@ -51,7 +51,10 @@ def log(msg):
 KERNEL_SOURCES = {
     "gram": ["gram.hip", "stream_common.h", "internal.h"],
     "combine": ["combine.hip", "combine_impl.h", "stream_common.h", "internal.h"],
-    "resident": ["resident.hip", "combine_impl.h", "solve_impl.h", "stream_common.h", "internal.h"],
+    "resident": ["resident.hip", "coop_common.h", "combine_impl.h", "solve_impl.h", "stream_common.h",
+                 "internal.h"],
+    "hybrid": ["hybrid.hip", "coop_common.h", "combine_impl.h", "solve_impl.h", "stream_common.h",
+               "internal.h"],
 }
 
 
@@ -114,7 +117,7 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--path", choices=["auto", "two-pass", "resident"], default="auto",
+    ap.add_argument("--path", choices=["auto", "two-pass", "resident", "hybrid"], default="auto",
                     help="force bkmoo_resolve's implementation (default: the library's choice)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run one plain elementwise kernel that reads 2 GiB and writes "
@@ -163,11 +166,15 @@ def main():
     W = torch.empty((B, K), dtype=torch.float32, device=dev)
     A = torch.empty((B, K), dtype=torch.float64, device=dev)
     stream = torch.cuda.current_stream(dev)
-    bkmoo.set_resolve_path({"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS,
-                            "resident": bkmoo.PATH_RESIDENT}[args.path])
+    bkmoo.set_resolve_path({"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS, "resident": bkmoo.PATH_RESIDENT,
+                            "hybrid": bkmoo.PATH_HYBRID}[args.path])
     path = bkmoo.resolve_path(grads, B + 1, wl.method, wl.max_iter)
-    resident = path == bkmoo.PATH_RESIDENT
-    log(f"resolve path: {'resident (single read)' if resident else 'two-pass'}")
+    path_name = {bkmoo.PATH_TWO_PASS: "two-pass", bkmoo.PATH_RESIDENT: "resident",
+                 bkmoo.PATH_HYBRID: "hybrid"}[path]
+    # the cooperative paths are one kernel: time the whole resolve call
+    resident = path in (bkmoo.PATH_RESIDENT, bkmoo.PATH_HYBRID)
+    traffic_bytes = bkmoo.resolve_traffic(K, wl.offsets(), wl.dtype, path)
+    log(f"resolve path: {path_name}; it moves {traffic_bytes / 1e9:.2f} GB of HBM traffic per step")
 
     def step(ev=None):
         if resident:
@@ -277,10 +284,11 @@ def main():
         f"{extras['gram_global_B1']:.3f} ms, per-bucket Gram {st.get('gram', float('nan')):.3f} ms")
     del ws8, P8, ws1
 
-    # dominant kernel: the resident kernel (reads K*s*N once, writes s*N), or
-    # the longer of the two streaming passes
+    # dominant kernel: the cooperative kernel (its own traffic: one read of
+    # the gradients, the re-read of what it did not keep, the update), or the
+    # longer of the two streaming passes
     if resident:
-        kname, kbytes, kms = "resident", (K + 1) * s * N, st["resolve"]
+        kname, kbytes, kms = path_name, traffic_bytes, st["resolve"]
     elif st["combine"] >= st["gram"]:
         kname, kbytes, kms = "combine", (K + 1) * s * N, st["combine"]
     else:
@@ -305,10 +313,11 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "K": K, "N": N, "B": B, "bucket_elems": wl.bucket_elems,
                    "method": wl.method, "max_iter": wl.max_iter, "cagrad_c": wl.cagrad_c},
-        "path": "resident" if resident else "two-pass",
+        "path": path_name,
         "stages_ms": {k: round(v, 4) for k, v in st.items()},
         "extras_ms": extras,
-        "resolve_algorithmic_GBps": round((2 * K + 1) * s * N / (ms_step / 1e3) / 1e9, 1),
+        "resolve_traffic_bytes": traffic_bytes,
+        "resolve_GBps": round(traffic_bytes / (ms_step / 1e3) / 1e9, 1),
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

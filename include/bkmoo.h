@@ -95,7 +95,9 @@ typedef enum {
 /* How bkmoo_resolve runs the step (bkmoo_resolve_path). */
 typedef enum {
   BKMOO_PATH_TWO_PASS = 1, /* Gram pass, solve, combine pass: reads the gradients twice */
-  BKMOO_PATH_RESIDENT = 2  /* one cooperative kernel, each bucket held on chip: reads them once */
+  BKMOO_PATH_RESIDENT = 2, /* one cooperative kernel, each bucket held on chip: reads them once */
+  BKMOO_PATH_HYBRID = 3    /* one cooperative kernel, half of each bucket held on chip, the next
+                              bucket's Gram overlapping this one's solve: ~(1.5K+1) reads */
 } bkmoo_path;
 
 /* Hyper-parameters of the solve step (host struct). */
@@ -297,6 +299,26 @@ bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *c
                              double *summary, int32_t *pairs, hipStream_t stream);
 
 /*
+ * bkmoo_resolve_traffic — the HBM bytes a bkmoo_resolve call moves on `path`
+ * (*bytes, host) for these bucket offsets (host array, int64 [B+1]): every
+ * gradient byte each pass reads plus the update written, counted from the
+ * path's own data movement:
+ *   BKMOO_PATH_TWO_PASS  2*K*s*N + s_out*N
+ *   BKMOO_PATH_RESIDENT  K*s*N + s_out*N, plus K*s per element of every bucket
+ *                        too large for the chip (read twice)
+ *   BKMOO_PATH_HYBRID    K*s*N + s_out*N, plus K*s per element a data
+ *                        workgroup did not keep on chip (read twice)
+ * with s, s_out the input and output element sizes.  The small per-bucket
+ * terms (offsets, Gram matrices, weights, partial sums) are left out.  The
+ * cooperative paths depend on the current device's CU count.  BKMOO_EINVAL
+ * for bad sizes or pointers, invalid offsets or an unknown path;
+ * BKMOO_EUNSUPPORTED for a cooperative path with K > 4; BKMOO_EHIP when the
+ * current device cannot be queried.
+ */
+bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_t *offsets_host,
+                                   bkmoo_dtype dt, bkmoo_dtype out_dt, int32_t path, uint64_t *bytes);
+
+/*
  * bkmoo_read_device_error — copy the workspace's device error word into
  * *err (host) after waiting for `stream`.  This call synchronises; it is a
  * diagnostic, not part of the hot path.  0 means the last call that used
@@ -314,8 +336,8 @@ bkmoo_status bkmoo_set_grid_override(int32_t workgroups);
 
 /*
  * bkmoo_resolve_path — the implementation bkmoo_resolve would use for these
- * arguments on the current device (*path, host): BKMOO_PATH_TWO_PASS or
- * BKMOO_PATH_RESIDENT.  `aligned` says whether every row and the output
+ * arguments on the current device (*path, host): BKMOO_PATH_TWO_PASS,
+ * BKMOO_PATH_RESIDENT or BKMOO_PATH_HYBRID.  `aligned` says whether every row and the output
  * start at the same 16-byte phase.
  */
 bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt, bkmoo_dtype out_dt,
@@ -324,8 +346,10 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
 
 /*
  * bkmoo_set_resolve_path — force bkmoo_resolve's implementation
- * (0: automatic, BKMOO_PATH_TWO_PASS, BKMOO_PATH_RESIDENT when eligible).
- * Process-wide; for tests and tuning.
+ * (0: automatic, BKMOO_PATH_TWO_PASS, BKMOO_PATH_RESIDENT or
+ * BKMOO_PATH_HYBRID when eligible: K <= 4, aligned rows, not an exact
+ * method; the hybrid path is taken only when forced).  Process-wide; for
+ * tests and tuning.
  */
 bkmoo_status bkmoo_set_resolve_path(int32_t path);
 

@@ -25,7 +25,7 @@ F32, BF16 = 0, 1
 METHODS = {"mgda": 0, "pcgrad": 1, "cagrad": 2, "mean": 3, "mgda-exact": 4, "cagrad-exact": 5}
 DEVERR_OFFSETS = 0x1
 DEVERR_TIMEOUT = 0x2
-PATH_TWO_PASS, PATH_RESIDENT = 1, 2
+PATH_TWO_PASS, PATH_RESIDENT, PATH_HYBRID = 1, 2, 3
 
 
 class BkmooError(RuntimeError):
@@ -52,6 +52,7 @@ def _load():
                           vp, ctypes.c_int, vp, vp, vp, vp, sz, vp],
         "bkmoo_conflicts": [i32, i32, vp, vp, vp, vp, vp],
         "bkmoo_slice_offsets": [i32, i32, vp, vp, vp],
+        "bkmoo_resolve_traffic": [i32, i64, i32, vp, ctypes.c_int, ctypes.c_int, i32, ctypes.POINTER(ctypes.c_uint64)],
         "bkmoo_gram_reduce": [i32, i32, i32, vp, ctypes.c_int, vp, vp],
         "bkmoo_read_device_error": [vp, ctypes.POINTER(u32), vp],
         "bkmoo_set_grid_override": [i32],
@@ -71,7 +72,8 @@ def _load():
 _lib = _load()
 
 EXPORTS = ("bkmoo_workspace_size", "bkmoo_gram", "bkmoo_solve", "bkmoo_combine", "bkmoo_resolve",
-           "bkmoo_conflicts", "bkmoo_slice_offsets", "bkmoo_gram_reduce", "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
+           "bkmoo_conflicts", "bkmoo_slice_offsets", "bkmoo_gram_reduce", "bkmoo_resolve_traffic",
+           "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
            "bkmoo_set_resolve_path", "bkmoo_set_wait_limit", "bkmoo_status_string")
 
 
@@ -306,7 +308,7 @@ def set_grid_override(workgroups: int):
 
 def resolve_path(grads: Grads, bucket_offsets_len: int, method: str = "mgda", max_iter: int = 20,
                  out_dtype=None) -> int:
-    """PATH_TWO_PASS or PATH_RESIDENT: what resolve() would run for these
+    """PATH_TWO_PASS, PATH_RESIDENT or PATH_HYBRID: what resolve() would run for these
     grads and method (output assumed aligned like the rows)."""
     arr, dt, K, N, dev, rows = _rows(grads)
     B = bucket_offsets_len - 1
@@ -318,8 +320,22 @@ def resolve_path(grads: Grads, bucket_offsets_len: int, method: str = "mgda", ma
     return out.value
 
 
+def resolve_traffic(K: int, bucket_offsets, dtype, path: int, out_dtype=None) -> int:
+    """HBM bytes a resolve on `path` moves for these offsets (a host int64
+    array-like of B+1 entries)."""
+    import numpy as np
+    offs = np.ascontiguousarray(np.asarray(bucket_offsets, dtype=np.int64))
+    code = lambda d: d if isinstance(d, int) else (F32 if d in (torch.float32, "f32") else BF16)
+    dt = code(dtype)
+    odt = dt if out_dtype is None else code(out_dtype)
+    out = ctypes.c_uint64(0)
+    _check(_lib.bkmoo_resolve_traffic(K, int(offs[-1]), len(offs) - 1, offs.ctypes.data, dt, odt, int(path),
+                                      ctypes.byref(out)), "bkmoo_resolve_traffic")
+    return out.value
+
+
 def set_resolve_path(path: int):
-    """0 automatic, PATH_TWO_PASS or PATH_RESIDENT (process-wide)."""
+    """0 automatic, PATH_TWO_PASS, PATH_RESIDENT or PATH_HYBRID (process-wide)."""
     _check(_lib.bkmoo_set_resolve_path(int(path)), "bkmoo_set_resolve_path")
 
 

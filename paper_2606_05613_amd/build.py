@@ -33,9 +33,10 @@ LIB = os.path.join(PKG, "libbkmoo.so")
 ARCH = "gfx950"
 
 SOURCES = ["api.hip", "schedule.hip", "gram.hip", "solve.hip", "solve_exact.hip", "combine.hip",
-           "resident.hip", "conflicts.hip", "slices.hip"]
+           "resident.hip", "hybrid.hip", "conflicts.hip", "slices.hip"]
 EXTRA = {"solve.hip": ["-ffp-contract=off"], "solve_exact.hip": ["-ffp-contract=off"],
-         "resident.hip": ["-ffp-contract=off"], "conflicts.hip": ["-ffp-contract=off"]}
+         "resident.hip": ["-ffp-contract=off"], "hybrid.hip": ["-ffp-contract=off"],
+         "conflicts.hip": ["-ffp-contract=off"]}
 
 
 def hipcc() -> str:

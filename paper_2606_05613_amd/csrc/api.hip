@@ -12,7 +12,7 @@ namespace bkmoo {
 namespace {
 
 std::atomic<int> g_grid_override{0};
-std::atomic<int> g_resolve_path{0};            // 0 automatic, 1 two-pass, 2 resident
+std::atomic<int> g_resolve_path{0};            // 0 automatic, 1 two-pass, 2 resident, 3 hybrid
 std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the resident path's bounded wait
 
 // Resident single-read resolve pays when a bucket is large enough to
@@ -123,7 +123,7 @@ Carved carve(void *ws, const Layout &L) {
 // Workgroups for the resident path, or 0 when it should not be used.
 int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters) {
   const int mode = g_resolve_path.load();
-  if (mode == 1 || K > 4 || !vec || is_exact(method)) return 0;
+  if (mode == 1 || mode == 3 || K > 4 || !vec || is_exact(method)) return 0;
   static std::atomic<int> cache[3][2][2];  // K-2, dt, out_dt (device model is fixed per process here)
   int g = cache[K - 2][dt][out_dt].load();
   if (g == 0) {
@@ -138,6 +138,41 @@ int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int m
   const bool cheap_solve = method == BKMOO_PCGRAD || method == BKMOO_MEAN || iters <= kResidentMaxIters;
   return B >= kResidentMinBuckets && bucket_bytes >= kResidentMinBucketBytes && avg_elems <= fits &&
                  cheap_solve
+             ? g
+             : 0;
+}
+
+// The pipelined, partly resident path pays when each bucket carries enough
+// data to cover the latency of its solve and weight hand-off (measured on
+// MI355X: buckets of 5 MiB per task run 2x slower than the two streaming
+// passes, 25 MiB ones 12% faster) and a fair share of each segment stays on
+// chip (100 MiB buckets keep 12% and lose to the two passes).
+constexpr int kHybridMinBuckets = 8;
+constexpr double kHybridMinBucketBytes = 48.0 * (1 << 20);  // all K rows
+constexpr double kHybridMinHeld = 0.3;                      // fraction of a bucket kept on chip
+
+// Workgroups for the pipelined, partly resident path, or 0 when it should
+// not be used.  Its partial Grams need two slots per data workgroup, and a
+// segment (about N / data workgroups elements at most) must stay within one
+// 32-bit buffer range.
+int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int64_t cap_slots) {
+  const int mode = g_resolve_path.load();
+  if (mode == 1 || mode == 2 || K > 4 || !vec || is_exact(method)) return 0;
+  static std::atomic<int> cache[3][2][2];  // K-2, dt, out_dt
+  int g = cache[K - 2][dt][out_dt].load();
+  if (g == 0) {
+    g = hybrid_grid(K, dt, out_dt);
+    cache[K - 2][dt][out_dt].store(g > 0 ? g : -1);
+  }
+  if (g <= 0) return 0;
+  const int gd = hybrid_data_workgroups(g);
+  if (2 * (int64_t)gd > cap_slots) return 0;
+  if ((N / gd + 2 * 4096) * (int64_t)elem_bytes(dt) >= ((int64_t)1 << 31)) return 0;
+  if (mode == 3) return g;
+  const double avg_elems = (double)N / B;
+  const double held = (double)hybrid_held_elems(K, dt) * gd / (avg_elems > 1.0 ? avg_elems : 1.0);
+  return B >= kHybridMinBuckets && avg_elems * K * elem_bytes(dt) >= kHybridMinBucketBytes &&
+                 held >= kHybridMinHeld
              ? g
              : 0;
 }
@@ -251,13 +286,24 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   const double c = hp ? hp->cagrad_c : 0.0;
   const int8_t *order = hp ? hp->pcgrad_order : nullptr;
 
+  const int hgrid =
+      choose_hybrid(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, L.cap_chunks);
+  if (hgrid > 0) {
+    hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start,
+                                   nullptr, w.err, w.sync, 2 * (int64_t)B * kSyncStride, stream);
+    if (e != hipSuccess) return BKMOO_EHIP;
+    e = launch_hybrid(K, (int)dt, (int)out_dt, grads, bucket_offsets, B, shift, (int)method, iters, c,
+                      order, G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride, w.err, g_spin_limit.load(),
+                      hgrid, stream);
+    return hip_status(e);
+  }
   const int rgrid = choose_resident(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters);
   if (rgrid > 0) {
     hipError_t e = launch_schedule(bucket_offsets, B, N, resident_segment_elems(K, dt), w.chunk_start,
-                                   nullptr, w.err, w.sync, 2 * (int64_t)B, stream);
+                                   nullptr, w.err, w.sync, 2 * (int64_t)B * kSyncStride, stream);
     if (e != hipSuccess) return BKMOO_EHIP;
     e = launch_resident(K, (int)dt, (int)out_dt, grads, bucket_offsets, w.chunk_start, B, shift,
-                        (int)method, iters, c, order, G, W, aux, out, w.partials, w.sync, w.sync + B,
+                        (int)method, iters, c, order, G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride,
                         w.err, g_spin_limit.load(), rgrid, stream);
     return hip_status(e);
   }
@@ -309,6 +355,52 @@ bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *c
   return hip_status(launch_conflicts(K, B, gram, cosines, summary, pairs, stream));
 }
 
+bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_t *offsets_host,
+                                   bkmoo_dtype dt, bkmoo_dtype out_dt, int32_t path, uint64_t *bytes) {
+  bkmoo_status st = check_shape(K, N, B, dt);
+  if (st != BKMOO_OK) return st;
+  if (!offsets_host || !bytes || !valid_dtype(out_dt)) return BKMOO_EINVAL;
+  if (offsets_host[0] != 0 || offsets_host[B] != N) return BKMOO_EINVAL;
+  for (int b = 0; b < B; ++b)
+    if (offsets_host[b + 1] < offsets_host[b]) return BKMOO_EINVAL;
+  const uint64_t s = (uint64_t)elem_bytes(dt), so = (uint64_t)elem_bytes(out_dt);
+  const uint64_t once = (uint64_t)K * s * (uint64_t)N + so * (uint64_t)N;
+  if (path == BKMOO_PATH_TWO_PASS) {
+    *bytes = once + (uint64_t)K * s * (uint64_t)N;
+    return BKMOO_OK;
+  }
+  if (path != BKMOO_PATH_RESIDENT && path != BKMOO_PATH_HYBRID) return BKMOO_EINVAL;
+  if (K > 4) return BKMOO_EUNSUPPORTED;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return BKMOO_EHIP;
+  uint64_t reread = 0;  // elements read a second time
+  if (path == BKMOO_PATH_RESIDENT) {
+    const int g = resident_grid(K, (int)dt, (int)out_dt);
+    if (g <= 0) return BKMOO_EUNSUPPORTED;
+    const int64_t seg = resident_segment_elems(K, (int)dt);
+    for (int b = 0; b < B; ++b) {  // a bucket with more segments than workgroups is read twice
+      const int64_t n = offsets_host[b + 1] - offsets_host[b];
+      if ((n + seg - 1) / seg > g) reread += (uint64_t)n;
+    }
+  } else {
+    const int g = hybrid_grid(K, (int)dt, (int)out_dt);
+    if (g <= 0) return BKMOO_EUNSUPPORTED;
+    const int gd = hybrid_data_workgroups(g);
+    const int64_t unit = hybrid_unit_elems((int)dt), held = hybrid_held_elems(K, (int)dt);
+    for (int b = 0; b < B; ++b) {  // each segment re-reads what it did not keep
+      const int64_t n = offsets_host[b + 1] - offsets_host[b];
+      int64_t len = (n + gd - 1) / gd;
+      len = (len + unit - 1) / unit * unit;
+      for (int64_t lo = 0; len > 0 && lo < n; lo += len) {
+        const int64_t m = lo + len < n ? len : n - lo;
+        if (m > held) reread += (uint64_t)(m - held);
+      }
+    }
+  }
+  *bytes = once + (uint64_t)K * s * reread;
+  return BKMOO_OK;
+}
+
 bkmoo_status bkmoo_read_device_error(const void *workspace, uint32_t *err, hipStream_t stream) {
   if (!workspace || !err) return BKMOO_EINVAL;
   uint32_t v = 0;
@@ -333,14 +425,18 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
   if (st != BKMOO_OK) return st;
   if (!valid_dtype(out_dt) || method < BKMOO_MGDA || method > BKMOO_CAGRAD_EXACT) return BKMOO_EINVAL;
   if (k_unsupported(K, method)) return BKMOO_EUNSUPPORTED;
-  *path = choose_resident(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter) > 0
-              ? BKMOO_PATH_RESIDENT
-              : BKMOO_PATH_TWO_PASS;
+  if (choose_hybrid(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method,
+                    layout(K, N, B, dt).cap_chunks) > 0)
+    *path = BKMOO_PATH_HYBRID;
+  else if (choose_resident(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter) > 0)
+    *path = BKMOO_PATH_RESIDENT;
+  else
+    *path = BKMOO_PATH_TWO_PASS;
   return BKMOO_OK;
 }
 
 bkmoo_status bkmoo_set_resolve_path(int32_t path) {
-  if (path < 0 || path > 2) return BKMOO_EINVAL;
+  if (path < 0 || path > 3) return BKMOO_EINVAL;
   g_resolve_path.store(path);
   return BKMOO_OK;
 }

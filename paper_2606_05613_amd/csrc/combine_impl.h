@@ -62,29 +62,6 @@ __device__ __forceinline__ float f32_round_odd(double d) {
 // sum_i w_i x_i for the output type ODT: an fp32 FMA chain for fp32
 // outputs; for bf16 outputs an fp64 chain rounded to odd into fp32 (the
 // store then rounds to nearest even).
-// The same V results through a buffer descriptor at byte offset voff+soff,
-// issued as 8-byte stores only.  A buffer store of more than 64 bits whose
-// scalar offset is a register reads its data VGPRs over two cycles, and the
-// compiler does not keep the next instruction from overwriting them there
-// (observed on gfx950 as sporadically wrong output lanes); 8-byte stores
-// have no such window.
-template <int ODT, int V>
-__device__ __forceinline__ void store_vec_buf(Rsrc r, uint32_t voff, uint32_t soff, const float *y) {
-  if constexpr (ODT == F32) {
-#pragma unroll
-    for (int q = 0; q < V / 2; ++q) {
-      u32x2 v = {__float_as_uint(y[2 * q]), __float_as_uint(y[2 * q + 1])};
-      buf_store8(v, r, voff + 8u * q, soff);
-    }
-  } else {
-#pragma unroll
-    for (int q = 0; q < V / 4; ++q) {
-      u32x2 v = {pack_bf16x2(y[4 * q], y[4 * q + 1]), pack_bf16x2(y[4 * q + 2], y[4 * q + 3])};
-      buf_store8(v, r, voff + 8u * q, soff);
-    }
-  }
-}
-
 template <int K, int ODT>
 __device__ __forceinline__ float wsum(const float *w, const float *x) {
   if constexpr (ODT == F32) {

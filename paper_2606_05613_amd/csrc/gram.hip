@@ -23,18 +23,6 @@ namespace bkmoo {
 
 namespace {
 
-template <int K>
-__device__ __forceinline__ void accumulate(float *acc, const float *x) {
-  int p = 0;
-#pragma unroll
-  for (int i = 0; i < K; ++i)
-#pragma unroll
-    for (int j = i; j < K; ++j) {
-      acc[p] = __builtin_fmaf(x[i], x[j], acc[p]);
-      ++p;
-    }
-}
-
 template <int K, int DT>
 __global__ __launch_bounds__(kThreads) void gram_partial_kernel(
     Rows<K> rows, const int64_t *__restrict__ offs, const int64_t *__restrict__ cs, int B,

@@ -1,0 +1,477 @@
+// Pipelined, partly resident resolve: one cooperative kernel in which the
+// Gram pass of bucket b+1 runs while the weights of bucket b are computed,
+// and each bucket is half held on chip between its Gram pass and its combine.
+//
+// Why.  The two-pass path reads every gradient twice, (2K+1)*s*N bytes.  The
+// single-read kernel holds a whole bucket on chip (a 25 MiB K=4 bf16 bucket
+// is ~60% of the chip's registers and LDS), so nothing else fits: every
+// workgroup idles while the bucket's Gram is reduced and its problem solved.
+// Holding about half of each workgroup's share of a bucket leaves room for two
+// buckets: the data of bucket b+1 streams in while bucket b's weights are
+// produced, and bucket b's combine re-reads only the part it did not keep.
+//
+// How.  Workgroups of 256 threads, two per CU (two can sit in different
+// phases, so one computes while the other streams).  The last kHybSolvers
+// workgroups of the grid hold no data: solver j
+// takes buckets j, j + kHybSolvers, ...; it waits until every data workgroup
+// has stored its partial Gram of the bucket, adds the partials in a fixed
+// order, solves on one wavefront and publishes the weights with a flag.  A
+// data workgroup w owns the w-th of at most GD equal segments of every bucket
+// (GD data workgroups; segments are whole multiples of one vector per
+// thread).  Of its segment it keeps the first NB = NR + NL vectors per task
+// row and thread in one of two buffers (registers and LDS) and streams the
+// rest.  Per workgroup the order is
+//   Gram(0) -> A, Gram(1) -> B, Combine(0) <- A, Gram(2) -> A, Combine(1) <- B, ...
+// A Gram phase computes the segment's partial Gram (the same fp32 arithmetic
+// and fixed-order reductions as the streaming pass), stores it in the
+// segment's slot and arrives at the bucket's counter.  A combine phase waits
+// for the bucket's flag (bounded) and writes the update from the buffer and
+// from a second read of the streamed part.
+//
+// No cycle of waits: a data workgroup waits for bucket b's weights only after
+// it has arrived for bucket b+1, every data workgroup arrives for bucket b
+// before it waits for bucket b-1's, and the solvers wait only for arrivals;
+// the cooperative launch keeps every workgroup resident.  Two sets of
+// partial slots suffice (bucket b uses set b & 1): a data workgroup writes
+// bucket b+2's partial in Gram(b+2), after its Combine(b) saw bucket b's
+// flag, which a solver sets only after it has read bucket b's partials.
+// Cross-workgroup data moves through the agent-scope primitives of
+// coop_common.h.
+//
+// The segment length depends on the number of data workgroups, so results
+// are reproducible on a given device but may differ in the last bits between
+// devices with different CU counts (unlike the streaming passes).
+#include "combine_impl.h"
+#include "coop_common.h"
+#include "solve_impl.h"
+
+namespace bkmoo {
+
+namespace {
+
+constexpr int kHybThreads = 256;  // two workgroups per CU
+constexpr int kHybWaves = kHybThreads / kWave;
+constexpr int kHybSolvers = 4;  // workgroups that reduce and solve, holding no data
+constexpr int kHybStream = 2;   // streamed vectors per task row and thread per step
+
+// Vectors per task row and thread kept in each of the two buffers: registers
+// (NR) and LDS (NL).  The two buffers together hold about what the
+// single-read kernel holds for one bucket.
+constexpr int hyb_regs(int K) { return K <= 2 ? 9 : K == 3 ? 6 : 4; }
+constexpr int hyb_lds(int K) { return K <= 2 ? 4 : 2; }
+
+struct HybArgs {
+  const int64_t *offs;  // [B+1]
+  int B;
+  int shift;
+  int method, iters;
+  double c;
+  const int8_t *order;
+  double *gram;      // [B][K][K]
+  float *weights;    // [B][K]
+  double *aux;       // [B][K] or null
+  void *out;
+  double *partials;  // [2][GD][P]: slot set b & 1 holds bucket b's segment partials
+  uint32_t *arrive;  // [B] at stride kSyncStride, zero at launch
+  uint32_t *flags;   // [B] at stride kSyncStride, zero at launch
+  uint32_t *err;
+  uint32_t spin_limit;
+};
+
+// Segment length of bucket b: ceil(n_b / GD) rounded up to `unit` elements.
+__device__ __forceinline__ int64_t seg_len(const int64_t *offs, int b, int GD, int64_t unit) {
+  const int64_t n = offs[b + 1] - offs[b];
+  const int64_t len = (n + GD - 1) / GD;
+  return (len + unit - 1) / unit * unit;
+}
+
+// Bounded wait until *p reaches `target` (thread 0 only); on timeout the
+// error word gets kErrTimeout and false is returned.
+__device__ bool wait_at_least(const uint32_t *p, uint32_t target, const HybArgs &a) {
+  uint32_t spins = 0;
+  while (load_agent(p) < target) {
+    __builtin_amdgcn_s_sleep(1);
+    if (++spins >= a.spin_limit) {
+      __hip_atomic_fetch_or(a.err, kErrTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return false;
+    }
+  }
+  return true;
+}
+
+template <int K, int DT, int ODT>
+struct Hybrid {
+  static constexpr int V = vec_elems(DT);
+  static constexpr int NR = hyb_regs(K);
+  static constexpr int NL = hyb_lds(K);
+  static constexpr int NB = NR + NL;
+  static constexpr int P = pairs(K);
+  static constexpr int T = kHybThreads;
+  static constexpr int EB = elem_bytes(DT);
+  static constexpr int NG = T / P;                     // reduction groups per Gram entry
+
+  struct Smem {
+    u32x4 lds[2][NL][K][T];
+    double red[kHybWaves][P];
+    double red2[P][NG];
+    Shared S;
+    float wsh[K];
+  };
+
+  // Gram phase of bucket b into buffer X (reg, hs and sm.lds[X]).
+  static __device__ __forceinline__ void gram(const Rows<K> &rows, const HybArgs &a, Smem &sm, int b, int w, int GD,
+                              int X, u32x4 (&reg)[NR][K], float (&hs)[K]) {
+    const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+    const int64_t len = seg_len(a.offs, b, GD, (int64_t)T * V);
+    const int64_t lo = a.offs[b] + (int64_t)w * len;
+    const int64_t hi = lo + len < a.offs[b + 1] ? lo + len : a.offs[b + 1];
+    const bool has = len > 0 && lo < hi;  // uniform over the workgroup
+    float acc[P];
+#pragma unroll
+    for (int p = 0; p < P; ++p) acc[p] = 0.0f;
+    if (has) {
+      const Split<V> sp(lo, hi, a.shift);
+      if (t < sp.nh + sp.nt) {
+        const int64_t n = t < sp.nh ? lo + t : sp.hi_a + (t - sp.nh);
+#pragma unroll
+        for (int i = 0; i < K; ++i) hs[i] = load_elem<DT>(rows.p[i], n);
+        accumulate<K>(acc, hs);
+      }
+      Rsrc rs[K];
+#pragma unroll
+      for (int i = 0; i < K; ++i)
+        rs[i] = make_rsrc(static_cast<const char *>(rows.p[i]) + sp.lo_a * EB, (uint32_t)sp.nv * 16u);
+      const uint32_t voff = (uint32_t)t * 16u;
+      // kept vectors (loads past the segment's last vector read zeros)
+#pragma unroll
+      for (int j = 0; j < NR; ++j) {
+#pragma unroll
+        for (int i = 0; i < K; ++i) reg[j][i] = buf_load16(rs[i], voff, (uint32_t)(j * T * 16));
+      }
+      {
+        u32x4 stage[NL][K];
+#pragma unroll
+        for (int j = 0; j < NL; ++j) {
+#pragma unroll
+          for (int i = 0; i < K; ++i) stage[j][i] = buf_load16(rs[i], voff, (uint32_t)((NR + j) * T * 16));
+        }
+#pragma unroll
+        for (int j = 0; j < NL; ++j) {
+#pragma unroll
+          for (int i = 0; i < K; ++i) sm.lds[X][j][i][t] = stage[j][i];
+        }
+      }
+      // streamed vectors, kHybStream per row at a time
+      const int nslot = (sp.nv + T - 1) / T;
+      for (int j0 = NB; j0 < nslot; j0 += kHybStream) {
+        u32x4 q[kHybStream][K];
+#pragma unroll
+        for (int u = 0; u < kHybStream; ++u) {
+#pragma unroll
+          for (int i = 0; i < K; ++i) q[u][i] = buf_load16(rs[i], voff, (uint32_t)((j0 + u) * T * 16));
+        }
+#pragma unroll
+        for (int u = 0; u < kHybStream; ++u) accumulate_vec(acc, q[u]);
+      }
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        u32x4 q[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) q[i] = j < NR ? reg[j < NR ? j : 0][i] : sm.lds[X][j < NR ? 0 : j - NR][i][t];
+        accumulate_vec(acc, q);
+      }
+    }
+    // fixed-order reduction: xor butterfly in the wave, waves in order
+#pragma unroll
+    for (int off = kWave / 2; off >= 1; off >>= 1) {
+#pragma unroll
+      for (int p = 0; p < P; ++p) acc[p] += __shfl_xor(acc[p], off, kWave);
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int p = 0; p < P; ++p) sm.red[wave][p] = (double)acc[p];
+    }
+    __syncthreads();
+    if (has && t < P) {
+      double v = sm.red[0][t];
+#pragma unroll
+      for (int q = 1; q < kHybWaves; ++q) v += sm.red[q][t];
+      store_agent(&a.partials[((int64_t)(b & 1) * GD + w) * P + t], v);
+    }
+    __syncthreads();
+    if (t == 0) {
+      wait_vm_complete();  // the slot (written by wave 0) is out
+      __hip_atomic_fetch_add(&a.arrive[(int64_t)b * kSyncStride], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+
+  static __device__ __forceinline__ void accumulate_vec(float (&acc)[P], const u32x4 (&q)[K]) {
+    float x[K][V];
+#pragma unroll
+    for (int i = 0; i < K; ++i) decode<DT>(q[i], x[i]);
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      float xe[K];
+#pragma unroll
+      for (int i = 0; i < K; ++i) xe[i] = x[i][e];
+      accumulate<K>(acc, xe);
+    }
+  }
+
+  // The update of one vector, stored with one 16-byte non-temporal global
+  // store (the lanes of a wavefront write 1 KiB contiguously) when v < nv.
+  static __device__ __forceinline__ void combine_vec(const float (&wv)[K], const u32x4 (&q)[K], void *out,
+                                                     int64_t first, bool in_range) {
+    float x[K][V];
+#pragma unroll
+    for (int i = 0; i < K; ++i) decode<DT>(q[i], x[i]);
+    float y[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      float xe[K];
+#pragma unroll
+      for (int i = 0; i < K; ++i) xe[i] = x[i][e];
+      y[e] = wsum<K, ODT>(wv, xe);
+    }
+    if (in_range) store_vec<ODT, V>(out, first, y);
+  }
+
+  // Combine phase of bucket b from buffer X.
+  static __device__ __forceinline__ void combine(const Rows<K> &rows, const HybArgs &a, Smem &sm, int b, int w, int GD,
+                                 int X, const u32x4 (&reg)[NR][K], const float (&hs)[K]) {
+    const int t = threadIdx.x;
+    if (t == 0) {
+      wait_at_least(&a.flags[(int64_t)b * kSyncStride], 1u, a);
+#pragma unroll
+      for (int i = 0; i < K; ++i) sm.wsh[i] = load_agent(&a.weights[(int64_t)b * K + i]);
+    }
+    __syncthreads();
+    float wv[K];
+#pragma unroll
+    for (int i = 0; i < K; ++i) wv[i] = sm.wsh[i];
+    const int64_t len = seg_len(a.offs, b, GD, (int64_t)T * V);
+    const int64_t lo = a.offs[b] + (int64_t)w * len;
+    const int64_t hi = lo + len < a.offs[b + 1] ? lo + len : a.offs[b + 1];
+    if (len > 0 && lo < hi) {
+      const Split<V> sp(lo, hi, a.shift);
+      if (t < sp.nh + sp.nt) {
+        const int64_t n = t < sp.nh ? lo + t : sp.hi_a + (t - sp.nh);
+        store_elem<ODT>(a.out, n, wsum<K, ODT>(wv, hs));
+      }
+      Rsrc rs[K];
+#pragma unroll
+      for (int i = 0; i < K; ++i)
+        rs[i] = make_rsrc(static_cast<const char *>(rows.p[i]) + sp.lo_a * EB, (uint32_t)sp.nv * 16u);
+      const uint32_t voff = (uint32_t)t * 16u;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        u32x4 q[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) q[i] = j < NR ? reg[j < NR ? j : 0][i] : sm.lds[X][j < NR ? 0 : j - NR][i][t];
+        const int v = j * T + t;
+        combine_vec(wv, q, a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
+      }
+      const int nslot = (sp.nv + T - 1) / T;
+      for (int j0 = NB; j0 < nslot; j0 += kHybStream) {
+        u32x4 q[kHybStream][K];
+#pragma unroll
+        for (int u = 0; u < kHybStream; ++u) {
+#pragma unroll
+          for (int i = 0; i < K; ++i) q[u][i] = buf_load16(rs[i], voff, (uint32_t)((j0 + u) * T * 16));
+        }
+#pragma unroll
+        for (int u = 0; u < kHybStream; ++u) {
+          const int v = (j0 + u) * T + t;
+          combine_vec(wv, q[u], a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
+        }
+      }
+    }
+  }
+
+  // Solver workgroup: buckets j, j + kHybSolvers, ... (j = w - GD).
+  static __device__ void solve(const HybArgs &a, Smem &sm, int w, int GD) {
+    const int t = threadIdx.x, wave = t / kWave;
+    __shared__ int ok_sh;
+    for (int b = w - GD; b < a.B; b += kHybSolvers) {
+      if (t == 0) ok_sh = wait_at_least(&a.arrive[(int64_t)b * kSyncStride], (uint32_t)GD, a) ? 1 : 0;
+      __syncthreads();
+      const int64_t len = seg_len(a.offs, b, GD, (int64_t)T * V);
+      const int64_t n = a.offs[b + 1] - a.offs[b];
+      const int64_t nseg = len > 0 ? (n + len - 1) / len : 0;
+      // segment slots in a fixed order: group g of entry p sums segments
+      // g, g+NG, ... ascending, then entry p sums its groups ascending
+      if (t < P * NG) {
+        const int p = t / NG, g = t % NG;
+        double v = 0.0;
+        for (int64_t s = g; s < nseg; s += 8 * NG) {  // 8 device-coherent loads in flight
+          double q[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int64_t ss = s + (int64_t)u * NG;
+            q[u] = ss < nseg ? load_agent(&a.partials[((int64_t)(b & 1) * GD + ss) * P + p]) : 0.0;
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v += q[u];
+        }
+        sm.red2[p][g] = v;
+      }
+      if (t == 0) sm.S.bad = ok_sh ? 0 : 1;
+      __syncthreads();
+      if (t < P) {
+        double v = 0.0;
+        for (int g = 0; g < NG; ++g) v += sm.red2[t][g];
+        int i = 0, rem = t;
+        while (rem >= K - i) {
+          rem -= K - i;
+          ++i;
+        }
+        const int j = i + rem;
+        sm.S.G[i * K + j] = v;
+        sm.S.G[j * K + i] = v;
+        a.gram[((int64_t)b * K + i) * K + j] = v;
+        a.gram[((int64_t)b * K + j) * K + i] = v;
+        if (!__builtin_isfinite(v)) sm.S.bad = 1;
+      }
+      __syncthreads();
+      if (wave == 0) {
+        double wt = 0.0, ax = 0.0;
+        if (a.method == PCGRAD || sm.S.bad) {
+          solver_run<WaveSync>(sm.S, K, a.method, a.iters, a.c, a.order, b, t, &wt, &ax);
+        } else {
+          double Gr[K][K], wr[K], xr[K];
+#pragma unroll
+          for (int i = 0; i < K; ++i)
+#pragma unroll
+            for (int j = 0; j < K; ++j) Gr[i][j] = sm.S.G[i * K + j];
+          if (a.method == MGDA) {
+            reg_solve_mgda<K>(Gr, a.iters, xr);
+#pragma unroll
+            for (int i = 0; i < K; ++i) wr[i] = xr[i];
+          } else if (a.method == CAGRAD) {
+            reg_solve_cagrad<K>(Gr, a.iters, a.c, wr, xr);
+          } else {
+#pragma unroll
+            for (int i = 0; i < K; ++i) wr[i] = xr[i] = 1.0 / (double)K;
+          }
+#pragma unroll
+          for (int i = 0; i < K; ++i)
+            if (t == i) {
+              wt = wr[i];
+              ax = xr[i];
+            }
+        }
+        if (t < K) {
+          store_agent(&a.weights[(int64_t)b * K + t], (float)wt);
+          if (a.aux) a.aux[(int64_t)b * K + t] = ax;
+        }
+        if (t == 0) {
+          wait_vm_complete();  // weights (written by this wavefront) are out
+          store_agent(&a.flags[(int64_t)b * kSyncStride], 1u);
+        }
+      }
+      __syncthreads();
+    }
+  }
+};
+
+template <int K, int DT, int ODT>
+__global__ __launch_bounds__(kHybThreads, 2) void hybrid_kernel(Rows<K> rows, HybArgs a) {
+  using H = Hybrid<K, DT, ODT>;
+  __shared__ typename H::Smem sm;
+  const int G = gridDim.x, GD = G - kHybSolvers, w = blockIdx.x;
+  if (*a.err & kErrOffsets) {
+    // the schedule rejected the offsets: NaN Gram and weights, no update
+    if (w == 0) {
+      const double nan = __builtin_nan("");
+      for (int64_t i = threadIdx.x; i < (int64_t)a.B * K * K; i += kHybThreads) a.gram[i] = nan;
+      for (int64_t i = threadIdx.x; i < (int64_t)a.B * K; i += kHybThreads) {
+        a.weights[i] = (float)nan;
+        if (a.aux) a.aux[i] = nan;
+      }
+    }
+    return;
+  }
+  if (w >= GD) {
+    H::solve(a, sm, w, GD);
+    return;
+  }
+  u32x4 regA[H::NR][K], regB[H::NR][K];
+  float hsA[K], hsB[K];
+  if (a.B > 0) H::gram(rows, a, sm, 0, w, GD, 0, regA, hsA);
+  for (int b = 0; b < a.B; b += 2) {
+    if (b + 1 < a.B) H::gram(rows, a, sm, b + 1, w, GD, 1, regB, hsB);
+    H::combine(rows, a, sm, b, w, GD, 0, regA, hsA);
+    if (b + 1 < a.B) {
+      if (b + 2 < a.B) H::gram(rows, a, sm, b + 2, w, GD, 0, regA, hsA);
+      H::combine(rows, a, sm, b + 1, w, GD, 1, regB, hsB);
+    }
+  }
+}
+
+template <int K, int DT, int ODT>
+hipError_t launch_hybrid_t(const void *const *row_ptrs, const HybArgs &a, int grid, hipStream_t s) {
+  Rows<K> rows;
+  for (int i = 0; i < K; ++i) rows.p[i] = row_ptrs[i];
+  HybArgs args = a;
+  void *kargs[] = {&rows, &args};
+  return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(&hybrid_kernel<K, DT, ODT>),
+                                    dim3((unsigned)grid), dim3(kHybThreads), kargs, 0, s);
+}
+
+template <int K, int DT, int ODT>
+int hybrid_grid_t() {
+  int occ = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, hybrid_kernel<K, DT, ODT>, kHybThreads, 0) !=
+      hipSuccess)
+    return 0;
+  const int g = occ * device_cu_count();
+  return g > 2 * kHybSolvers ? g : 0;
+}
+
+}  // namespace
+
+int hybrid_grid(int K, int dt, int out_dt) {
+#define BKMOO_HYB_CASE(k)                                                                           \
+  case k:                                                                                           \
+    if (dt == F32) return out_dt == F32 ? hybrid_grid_t<k, F32, F32>() : hybrid_grid_t<k, F32, BF16>(); \
+    return out_dt == F32 ? hybrid_grid_t<k, BF16, F32>() : hybrid_grid_t<k, BF16, BF16>();
+  switch (K) {
+    BKMOO_HYB_CASE(2)
+    BKMOO_HYB_CASE(3)
+    BKMOO_HYB_CASE(4)
+    default: return 0;
+  }
+#undef BKMOO_HYB_CASE
+}
+
+int hybrid_data_workgroups(int grid) { return grid - kHybSolvers; }
+
+int64_t hybrid_held_elems(int K, int dt) {
+  return (int64_t)kHybThreads * (hyb_regs(K) + hyb_lds(K)) * vec_elems(dt);
+}
+
+int64_t hybrid_unit_elems(int dt) { return (int64_t)kHybThreads * vec_elems(dt); }
+
+hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
+                         int shift, int method, int iters, double c, const int8_t *order, double *gram,
+                         float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
+                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid, hipStream_t s) {
+  const HybArgs a{offs, B, shift, method, iters, c, order, gram, weights, aux, out,
+                  partials, arrive, flags, err, spin_limit};
+#define BKMOO_HYB_CASE(k)                                                                        \
+  case k:                                                                                        \
+    if (dt == F32)                                                                               \
+      return out_dt == F32 ? launch_hybrid_t<k, F32, F32>(rows, a, grid, s)                      \
+                           : launch_hybrid_t<k, F32, BF16>(rows, a, grid, s);                    \
+    return out_dt == F32 ? launch_hybrid_t<k, BF16, F32>(rows, a, grid, s)                       \
+                         : launch_hybrid_t<k, BF16, BF16>(rows, a, grid, s);
+  switch (K) {
+    BKMOO_HYB_CASE(2)
+    BKMOO_HYB_CASE(3)
+    BKMOO_HYB_CASE(4)
+    default: return hipErrorInvalidValue;
+  }
+#undef BKMOO_HYB_CASE
+}
+
+}  // namespace bkmoo

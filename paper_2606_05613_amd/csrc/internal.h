@@ -51,6 +51,16 @@ constexpr int pairs(int K) { return K * (K + 1) / 2; }
 // order: the summation order depends only on the bucket's chunk count.
 constexpr int kFinalizeGroup = 1024;
 
+// Partial-Gram slots the workspace always has room for (the pipelined
+// cooperative kernel uses two sets, one per workgroup that holds data).
+constexpr int64_t kCoopSlots = 1024;
+
+// The cooperative kernels' per-bucket arrival counters and flags sit 128
+// bytes apart (one per cache line): with 4-byte neighbours, device-scope
+// atomics on one bucket's counter and polls of the next buckets' counters
+// contend for the same line (measured: 1.4 ms of a 23 ms step).
+constexpr int64_t kSyncStride = 32;  // uint32 words
+
 // Workspace layout (every region 256-byte aligned):
 //   [0, 256)            header: uint32 error word at byte 0
 //   chunk_start         int64 [B + 1]     (prefix sum of chunks per bucket)
@@ -59,7 +69,7 @@ constexpr int kFinalizeGroup = 1024;
 //   partials            fp64  [cap][P]    cap = ceil(N / C) + B
 //   group_start         int64 [B + 1]     (prefix sum of finalize groups per bucket)
 //   groups              fp64  [gcap][P]   gcap = cap / kFinalizeGroup + B + 1
-//   sync                uint32 [2][B]     resident path: arrival counters, flags
+//   sync                uint32 [2][B][kSyncStride]  cooperative paths: arrival counters, flags
 struct Layout {
   size_t err, chunk_start, gram, weights, partials, group_start, groups, sync, total;
   int64_t cap_chunks, cap_groups;
@@ -71,6 +81,8 @@ inline Layout layout(int K, int64_t N, int B, int dt) {
   Layout L;
   const int64_t C = gram_chunk_elems(K, dt);  // the smallest chunk with partial slots
   L.cap_chunks = (N + C - 1) / C + B;
+  // at least two sets of slots for up to 512 workgroups of a cooperative kernel
+  if (L.cap_chunks < kCoopSlots) L.cap_chunks = kCoopSlots;
   size_t o = 0;
   L.err = o;            o += 256;
   L.chunk_start = o;    o = align256(o + sizeof(int64_t) * (size_t)(B + 1));
@@ -80,7 +92,7 @@ inline Layout layout(int K, int64_t N, int B, int dt) {
   L.cap_groups = L.cap_chunks / kFinalizeGroup + B + 1;
   L.group_start = o;    o = align256(o + sizeof(int64_t) * (size_t)(B + 1));
   L.groups = o;         o = align256(o + sizeof(double) * (size_t)L.cap_groups * pairs(K));
-  L.sync = o;           o = align256(o + sizeof(uint32_t) * 2 * (size_t)B);
+  L.sync = o;           o = align256(o + sizeof(uint32_t) * 2 * (size_t)B * kSyncStride);
   L.total = o;
   return L;
 }
@@ -144,6 +156,20 @@ hipError_t launch_resident(int K, int dt, int out_dt, const void *const *rows, c
                            const int8_t *order, double *gram, float *weights, double *aux, void *out,
                            double *partials, uint32_t *arrive, uint32_t *flags, uint32_t *err,
                            uint32_t spin_limit, int grid, hipStream_t s);
+
+// Pipelined, partly resident resolve (K <= 4): cooperative grid (0 if the
+// combination cannot run this way), and how many of its workgroups hold data
+// (the rest solve); partials must hold 2 * data workgroups slots.
+int hybrid_grid(int K, int dt, int out_dt);
+int hybrid_data_workgroups(int grid);
+// Elements of its segment a data workgroup keeps on chip per bucket, and the
+// granule segment lengths are rounded up to.
+int64_t hybrid_held_elems(int K, int dt);
+int64_t hybrid_unit_elems(int dt);
+hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
+                         int shift, int method, int iters, double c, const int8_t *order, double *gram,
+                         float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
+                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid, hipStream_t s);
 
 int device_cu_count();
 

@@ -34,6 +34,7 @@
 // would instead write back or invalidate a whole XCD's L2 per workgroup and
 // bucket.
 #include "combine_impl.h"
+#include "coop_common.h"
 #include "solve_impl.h"
 
 namespace bkmoo {
@@ -69,36 +70,11 @@ struct ResArgs {
   double *aux;               // [B][K] or null
   void *out;
   double *partials;          // [segments][P]
-  uint32_t *arrive;          // [B], zero at launch
-  uint32_t *flags;           // [B], zero at launch
+  uint32_t *arrive;          // [B] at stride kSyncStride, zero at launch
+  uint32_t *flags;           // [B] at stride kSyncStride, zero at launch
   uint32_t *err;
   uint32_t spin_limit;
 };
-
-// Wait until every vector memory access this wavefront issued has completed
-// (vmcnt = 0; expcnt and lgkmcnt left unconstrained).
-__device__ __forceinline__ void wait_vm_complete() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
-template <typename T>
-__device__ __forceinline__ void store_agent(T *p, T v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-template <typename T>
-__device__ __forceinline__ T load_agent(const T *p) {
-  return __hip_atomic_load(const_cast<T *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-template <int K>
-__device__ __forceinline__ void accumulate(float *acc, const float *x) {
-  int p = 0;
-#pragma unroll
-  for (int i = 0; i < K; ++i)
-#pragma unroll
-    for (int j = i; j < K; ++j) {
-      acc[p] = __builtin_fmaf(x[i], x[j], acc[p]);
-      ++p;
-    }
-}
 
 template <int K, int DT, int ODT>
 __global__ __launch_bounds__(kResThreads, 1) void resident_kernel(Rows<K> rows, ResArgs a) {
@@ -224,7 +200,7 @@ __global__ __launch_bounds__(kResThreads, 1) void resident_kernel(Rows<K> rows, 
     if (t == 0) {
       wait_vm_complete();  // this workgroup's segment slots (written by wave 0) are out
       const uint32_t old =
-          __hip_atomic_fetch_add(&a.arrive[b], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_fetch_add(&a.arrive[(int64_t)b * kSyncStride], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       last_sh = old == (uint32_t)G - 1;
     }
     __syncthreads();
@@ -299,14 +275,14 @@ __global__ __launch_bounds__(kResThreads, 1) void resident_kernel(Rows<K> rows, 
         }
         if (t == 0) {
           wait_vm_complete();  // weights (written by this wavefront) are out
-          store_agent(&a.flags[b], 1u);
+          store_agent(&a.flags[(int64_t)b * kSyncStride], 1u);
         }
       }
       __syncthreads();
     } else {
       if (t == 0) {
         uint32_t spins = 0;
-        while (load_agent(&a.flags[b]) == 0u) {
+        while (load_agent(&a.flags[(int64_t)b * kSyncStride]) == 0u) {
           __builtin_amdgcn_s_sleep(1);
           if (++spins >= a.spin_limit) {
             __hip_atomic_fetch_or(a.err, kErrTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -339,9 +315,6 @@ __global__ __launch_bounds__(kResThreads, 1) void resident_kernel(Rows<K> rows, 
 #pragma unroll
       for (int i = 0; i < K; ++i)
         rs[i] = make_rsrc(static_cast<const char *>(rows.p[i]) + sp.lo_a * EB, (uint32_t)sp.nv * 16u);
-      constexpr int OB = V * (ODT == F32 ? 4 : 2);  // output bytes per vector
-      const Rsrc ro = make_rsrc(static_cast<char *>(a.out) + sp.lo_a * (ODT == F32 ? 4 : 2),
-                                (uint32_t)sp.nv * OB);
 #pragma unroll
       for (int j = 0; j < NR + NL; ++j) {
         u32x4 q[K];
@@ -362,7 +335,9 @@ __global__ __launch_bounds__(kResThreads, 1) void resident_kernel(Rows<K> rows, 
           for (int i = 0; i < K; ++i) xe[i] = x[i][e];
           y[e] = wsum<K, ODT>(wv, xe);
         }
-        store_vec_buf<ODT, V>(ro, (uint32_t)t * OB, (uint32_t)(j * T * OB), y);
+        // one 16-byte non-temporal global store per vector: the lanes of a
+        // wavefront write 1 KiB contiguously
+        if (j * T + t < sp.nv) store_vec<ODT, V>(a.out, sp.lo_a + (int64_t)(j * T + t) * V, y);
       }
     }
     __syncthreads();  // LDS slots and shared scratch are reused by the next bucket

@@ -155,6 +155,20 @@ def test_slice_argument_errors(b):
     assert L.bkmoo_gram_reduce(4, 3, 2, None, 0, g, None) == -1
 
 
+def test_resolve_traffic_two_pass_and_errors(b):
+    """The two-pass byte count needs no device: 2K reads and one write per
+    element; bad offsets and unknown paths are rejected."""
+    import numpy as np
+    offs = np.array([0, 10, 25, 25, 40])
+    assert b.resolve_traffic(4, offs, "bf16", b.PATH_TWO_PASS) == (2 * 4 * 2 + 2) * 40
+    assert b.resolve_traffic(3, offs, "f32", b.PATH_TWO_PASS, out_dtype="bf16") == (2 * 3 * 4 + 2) * 40
+    for bad in ([0, 10, 5, 40], [1, 10, 40]):
+        with pytest.raises(b.BkmooError, match="EINVAL"):
+            b.resolve_traffic(4, np.array(bad), "bf16", b.PATH_TWO_PASS)
+    with pytest.raises(b.BkmooError, match="EINVAL"):
+        b.resolve_traffic(4, offs, "bf16", 7)
+
+
 def test_grid_override_rejects_negative(b):
     assert b._lib.bkmoo_set_grid_override(-1) == -1
     assert b._lib.bkmoo_set_grid_override(0) == 0

@@ -1,7 +1,10 @@
-"""The single-read (resident) resolve against the oracle: every method and
-input type for K = 2..4, ragged and unaligned buckets, a bucket larger than
-the chip holds (two reads), determinism, agreement with the two-pass path,
-and the bounded wait's timeout forced from the host."""
+"""The two cooperative resolve kernels against the oracle: the single-read
+(resident) kernel and the pipelined, partly resident (hybrid) one.  Every
+method and input type for K = 2..4, ragged and unaligned buckets, 1 to 41
+buckets (the hybrid kernel alternates two buffers), full 25 MiB buckets
+(whose hybrid segments stream part of their data), a bucket larger than the
+chip holds, determinism, agreement with the two-pass path, and the bounded
+waits' timeout forced from the host."""
 
 import numpy as np
 import pytest
@@ -18,10 +21,12 @@ BASE = WORKLOADS["llama3-8b-k4-mgda-bf16"]
 LENS = [70_001, 1, 0, 33_333, 131_072, 7, 65_539, 40_047]
 
 
-@pytest.fixture
-def resident(gpu_lib):
-    gpu_lib.set_resolve_path(gpu_lib.PATH_RESIDENT)
-    yield gpu_lib
+@pytest.fixture(params=["resident", "hybrid"])
+def coop(request, gpu_lib):
+    """The library with one of the cooperative paths forced, and that path."""
+    path = {"resident": gpu_lib.PATH_RESIDENT, "hybrid": gpu_lib.PATH_HYBRID}[request.param]
+    gpu_lib.set_resolve_path(path)
+    yield gpu_lib, path
     gpu_lib.set_resolve_path(0)
 
 
@@ -35,32 +40,56 @@ def two_pass(gpu_lib):
 @pytest.mark.parametrize("method", ["mgda", "pcgrad", "cagrad", "mean"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("K", [2, 3, 4])
-def test_resident_parity(resident, method, dtype, K):
+def test_coop_parity(coop, method, dtype, K):
+    lib, path = coop
     wl = small_workload(BASE, sum(LENS), bucket_lens=LENS, K=K, dtype=dtype, method=method,
                         seed=9000 + 10 * K + (dtype == "bf16"))
     grads, _, _ = to_device_inputs(wl)
-    assert resident.resolve_path(grads, wl.B + 1, method) == resident.PATH_RESIDENT
-    print(f"case {wl.name} K={K} {dtype} {method}", full_parity(resident, wl, grads=grads), flush=True)
+    assert lib.resolve_path(grads, wl.B + 1, method) == path
+    print(f"case path {path} {wl.name} K={K} {dtype} {method}", full_parity(lib, wl, grads=grads), flush=True)
 
 
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
-def test_resident_output_types(resident, out_dtype):
+def test_coop_output_types(coop, out_dtype):
+    lib, _ = coop
     wl = small_workload(BASE, 200_000, bucket_lens=[99_999, 100_001], K=3, dtype="bf16", seed=77)
-    print(full_parity(resident, wl, out_dtype=out_dtype), flush=True)
+    print(full_parity(lib, wl, out_dtype=out_dtype), flush=True)
 
 
-def test_resident_bucket_larger_than_chip(resident):
-    """One K=2 fp32 bucket of 14.5M elements exceeds 256 workgroups x one
-    segment, so workgroups hold several segments and re-read them."""
+@pytest.mark.parametrize("nb", [1, 2, 3, 41])
+def test_coop_bucket_counts(coop, nb):
+    """Odd and even bucket counts through the two-buffer pipeline."""
+    lib, path = coop
+    rng = np.random.default_rng(nb)
+    lens = [int(x) for x in rng.integers(1, 90_000, size=nb)]
+    wl = small_workload(BASE, sum(lens), bucket_lens=lens, K=4, dtype="bf16", method="mgda", seed=600 + nb)
+    print(f"case path {path} B={nb}", full_parity(lib, wl), flush=True)
+
+
+def test_coop_full_size_buckets(coop):
+    """Three 25 MiB-per-task K=4 bf16 buckets: the hybrid kernel keeps part
+    of each segment and streams the rest twice."""
+    lib, path = coop
+    wl = small_workload(BASE, 3 * 13_107_200, bucket_elems=13_107_200, K=4, dtype="bf16", method="mgda",
+                        seed=620)
+    print(f"case path {path} 3 x 25 MiB", full_parity(lib, wl), flush=True)
+
+
+def test_coop_bucket_larger_than_chip(coop):
+    """One K=2 fp32 bucket of 14.5M elements: the resident kernel's
+    workgroups hold several segments and re-read them; the hybrid kernel's
+    segments stream most of their data."""
+    lib, _ = coop
     wl = small_workload(WORKLOADS["k2-mgda-1m-f32"], 14_500_000, bucket_lens=[14_500_000], seed=5)
-    print(full_parity(resident, wl), flush=True)
+    print(full_parity(lib, wl), flush=True)
 
 
-def test_resident_deterministic_and_close_to_two_pass(gpu_lib):
+@pytest.mark.parametrize("path_name", ["PATH_RESIDENT", "PATH_HYBRID"])
+def test_coop_deterministic_and_close_to_two_pass(gpu_lib, path_name):
     wl = small_workload(BASE, sum(LENS), bucket_lens=LENS, K=4, dtype="bf16", method="cagrad", seed=31)
     grads, offs, order = to_device_inputs(wl)
     try:
-        gpu_lib.set_resolve_path(gpu_lib.PATH_RESIDENT)
+        gpu_lib.set_resolve_path(getattr(gpu_lib, path_name))
         r1 = run_resolve(gpu_lib, wl, grads, offs, order)
         r2 = run_resolve(gpu_lib, wl, grads, offs, order)
         gpu_lib.set_resolve_path(gpu_lib.PATH_TWO_PASS)
@@ -74,18 +103,19 @@ def test_resident_deterministic_and_close_to_two_pass(gpu_lib):
     np.testing.assert_allclose(r1["weights"], r3["weights"], rtol=0, atol=1e-5)
 
 
-def test_resident_wait_timeout_forced_from_host(resident):
+def test_coop_wait_timeout_forced_from_host(coop):
     """A one-poll wait limit makes waiting workgroups give up at once: the
     call still completes (no hang) and, if any wait expired, says so."""
+    lib, _ = coop
     wl = small_workload(BASE, sum(LENS), bucket_lens=LENS, K=4, dtype="bf16", seed=41)
     grads, offs, _ = to_device_inputs(wl)
-    ws = torch.empty(resident.workspace_size(wl.K, wl.N, wl.B, "bf16"), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(lib.workspace_size(wl.K, wl.N, wl.B, "bf16"), dtype=torch.uint8, device="cuda")
     try:
-        resident.set_wait_limit(1)
-        resident.resolve(grads, offs, "mgda", workspace=ws)
-        err = resident.read_device_error(ws)
+        lib.set_wait_limit(1)
+        lib.resolve(grads, offs, "mgda", workspace=ws)
+        err = lib.read_device_error(ws)
     finally:
-        resident.set_wait_limit(1 << 22)
-    assert err in (0, resident.DEVERR_TIMEOUT)
-    resident.resolve(grads, offs, "mgda", workspace=ws)
-    assert resident.read_device_error(ws) == 0
+        lib.set_wait_limit(1 << 22)
+    assert err in (0, lib.DEVERR_TIMEOUT)
+    lib.resolve(grads, offs, "mgda", workspace=ws)
+    assert lib.read_device_error(ws) == 0
