@@ -16,9 +16,13 @@ Reported next to the throughput:
   roofline     the longest kernel of a step (HBM-bound), timed with HIP
                events on its launch stream inside the timed region:
                algorithmic bytes per launch / average launch duration,
-               against MI355X's 8 TB/s; `traffic` comes from the committed
-               rocprofv3 counter summary when it matches the current kernel
-               source, else null;
+               against MI355X's 8 TB/s.  A streaming pass counts the bytes
+               it must move (Gram K*s*N, combine (K+1)*s*N); a cooperative
+               kernel, which does the whole step, counts the one-read floor
+               K*s*N + s_out*N and gets no credit for its re-reads, part of
+               which the last-level cache serves.  `traffic` (HBM bytes per
+               launch) comes from the committed rocprofv3 counter summary
+               when it matches the current kernel source, else null;
   cpu_baseline the float64 oracle on a bounded prefix of the same buckets,
                on this host's cores.
 """
@@ -174,7 +178,7 @@ def main():
     # the cooperative paths are one kernel: time the whole resolve call
     resident = path in (bkmoo.PATH_RESIDENT, bkmoo.PATH_HYBRID)
     traffic_bytes = bkmoo.resolve_traffic(K, wl.offsets(), wl.dtype, path)
-    log(f"resolve path: {path_name}; it moves {traffic_bytes / 1e9:.2f} GB of HBM traffic per step")
+    log(f"resolve path: {path_name}; it requests {traffic_bytes / 1e9:.2f} GB from memory per step")
 
     def step(ev=None):
         if resident:
@@ -284,11 +288,11 @@ def main():
         f"{extras['gram_global_B1']:.3f} ms, per-bucket Gram {st.get('gram', float('nan')):.3f} ms")
     del ws8, P8, ws1
 
-    # dominant kernel: the cooperative kernel (its own traffic: one read of
-    # the gradients, the re-read of what it did not keep, the update), or the
-    # longer of the two streaming passes
+    # dominant kernel: the cooperative kernel (credited with the one-read
+    # floor: the gradients once and the update), or the longer of the two
+    # streaming passes
     if resident:
-        kname, kbytes, kms = path_name, traffic_bytes, st["resolve"]
+        kname, kbytes, kms = path_name, (K + 1) * s * N, st["resolve"]
     elif st["combine"] >= st["gram"]:
         kname, kbytes, kms = "combine", (K + 1) * s * N, st["combine"]
     else:
@@ -316,8 +320,8 @@ def main():
         "path": path_name,
         "stages_ms": {k: round(v, 4) for k, v in st.items()},
         "extras_ms": extras,
-        "resolve_traffic_bytes": traffic_bytes,
-        "resolve_GBps": round(traffic_bytes / (ms_step / 1e3) / 1e9, 1),
+        "resolve_requested_bytes": traffic_bytes,
+        "resolve_requested_GBps": round(traffic_bytes / (ms_step / 1e3) / 1e9, 1),
         "roofline": roof,
     }
     if not args.no_cpu_baseline:

@@ -299,10 +299,12 @@ bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *c
                              double *summary, int32_t *pairs, hipStream_t stream);
 
 /*
- * bkmoo_resolve_traffic — the HBM bytes a bkmoo_resolve call moves on `path`
- * (*bytes, host) for these bucket offsets (host array, int64 [B+1]): every
- * gradient byte each pass reads plus the update written, counted from the
- * path's own data movement:
+ * bkmoo_resolve_traffic — the bytes a bkmoo_resolve call requests from
+ * memory on `path` (*bytes, host) for these bucket offsets (host array,
+ * int64 [B+1]): every gradient byte each pass reads plus the update written,
+ * counted from the path's own data movement.  On the hybrid path part of the
+ * second read of a streamed element is served by the last-level cache, so
+ * its HBM bytes are lower; on the others all of it comes from HBM:
  *   BKMOO_PATH_TWO_PASS  2*K*s*N + s_out*N
  *   BKMOO_PATH_RESIDENT  K*s*N + s_out*N, plus K*s per element of every bucket
  *                        too large for the chip (read twice)

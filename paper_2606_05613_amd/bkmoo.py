@@ -321,8 +321,9 @@ def resolve_path(grads: Grads, bucket_offsets_len: int, method: str = "mgda", ma
 
 
 def resolve_traffic(K: int, bucket_offsets, dtype, path: int, out_dtype=None) -> int:
-    """HBM bytes a resolve on `path` moves for these offsets (a host int64
-    array-like of B+1 entries)."""
+    """Bytes a resolve on `path` requests from memory for these offsets (a
+    host int64 array-like of B+1 entries); on the hybrid path part of the
+    re-read is served by the last-level cache."""
     import numpy as np
     offs = np.ascontiguousarray(np.asarray(bucket_offsets, dtype=np.int64))
     code = lambda d: d if isinstance(d, int) else (F32 if d in (torch.float32, "f32") else BF16)

@@ -78,6 +78,13 @@ struct HybArgs {
   uint32_t spin_limit;
 };
 
+// buf_load16 with the default (temporal) cache policy: the line may stay in
+// the last-level cache (the 256 MB Infinity Cache), which pays off for data
+// read again soon after.
+__device__ __forceinline__ u32x4 buf_load16_keep(Rsrc r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+}
+
 // Segment length of bucket b: ceil(n_b / GD) rounded up to `unit` elements.
 __device__ __forceinline__ int64_t seg_len(const int64_t *offs, int b, int GD, int64_t unit) {
   const int64_t n = offs[b + 1] - offs[b];
@@ -161,14 +168,16 @@ struct Hybrid {
           for (int i = 0; i < K; ++i) sm.lds[X][j][i][t] = stage[j][i];
         }
       }
-      // streamed vectors, kHybStream per row at a time
+      // streamed vectors, kHybStream per row at a time; loaded with the
+      // temporal policy so that the combine's re-read, one bucket later, is
+      // mostly served by the last-level cache instead of HBM
       const int nslot = (sp.nv + T - 1) / T;
       for (int j0 = NB; j0 < nslot; j0 += kHybStream) {
         u32x4 q[kHybStream][K];
 #pragma unroll
         for (int u = 0; u < kHybStream; ++u) {
 #pragma unroll
-          for (int i = 0; i < K; ++i) q[u][i] = buf_load16(rs[i], voff, (uint32_t)((j0 + u) * T * 16));
+          for (int i = 0; i < K; ++i) q[u][i] = buf_load16_keep(rs[i], voff, (uint32_t)((j0 + u) * T * 16));
         }
 #pragma unroll
         for (int u = 0; u < kHybStream; ++u) accumulate_vec(acc, q[u]);
@@ -271,6 +280,7 @@ struct Hybrid {
         const int v = j * T + t;
         combine_vec(wv, q, a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
       }
+      // the re-read is the data's last use: streaming policy
       const int nslot = (sp.nv + T - 1) / T;
       for (int j0 = NB; j0 < nslot; j0 += kHybStream) {
         u32x4 q[kHybStream][K];
