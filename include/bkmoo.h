@@ -219,7 +219,19 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  *             fixed, grid-independent) order, so results agree with the
  *             two-pass path to rounding, not bitwise.  A bucket larger than
  *             the chip holds is read twice, still correct.
- * The resident path is chosen when the call has at least 32 buckets, the
+ *   hybrid    (K <= 4, aligned as above) one cooperative kernel in which
+ *             the Gram pass of bucket b+1 runs while bucket b is solved;
+ *             about half of each bucket stays on chip between its Gram and
+ *             its combine and the rest is read again (mostly from the
+ *             last-level cache).  Same agreement with the two-pass path as
+ *             the resident one; results depend on the device's CU count.
+ * The hybrid path is chosen first: for at least 8 buckets averaging at
+ * least 48 MiB (all K rows) of which at least 10% stays on chip, and a
+ * solve whose estimated latency (0.07 K us per MGDA iteration, 0.22 K us
+ * per CAGrad iteration, 0.1 K^2 us for PCGrad, 0 for the mean) is at most
+ * 1.5 times the time the next bucket's Gram read takes at 7 TB/s, so
+ * that it hides behind it.  Exact solvers never take a cooperative path.
+ * Else the resident path is chosen when the call has at least 32 buckets, the
  * average bucket holds at least 32 MiB of gradients and fits on chip, and
  * the solve is short (PCGrad, mean, or at most 2 Frank-Wolfe iterations):
  * each bucket's solve lies on the resident kernel's critical path, and the

@@ -143,19 +143,40 @@ int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int m
 }
 
 // The pipelined, partly resident path pays when each bucket carries enough
-// data to cover the latency of its solve and weight hand-off (measured on
-// MI355X: buckets of 5 MiB per task run 2x slower than the two streaming
-// passes, 25 MiB ones 12% faster) and a fair share of each segment stays on
-// chip (100 MiB buckets keep 12% and lose to the two passes).
+// data to cover the latency of its solve and weight hand-off and a fair
+// share of each segment stays on chip.  Measured on MI355X (K = 2..4 bf16,
+// 2G elements, MGDA FW-20): buckets of 8 MiB per task run 22% slower than
+// the two streaming passes, 12 MiB ones tie, 16-50 MiB ones are 11-21%
+// faster, 100 MiB ones (12% kept on chip) 4% faster, and 200 or 400 MiB
+// ones (6-8% kept) 3-9% slower.
 constexpr int kHybridMinBuckets = 8;
 constexpr double kHybridMinBucketBytes = 48.0 * (1 << 20);  // all K rows
-constexpr double kHybridMinHeld = 0.3;                      // fraction of a bucket kept on chip
+constexpr double kHybridMinHeld = 0.1;                      // fraction of a bucket kept on chip
+
+// A bucket's solve runs on one wavefront while the data workgroups stream
+// the next bucket; what it cannot hide stalls every workgroup.  Estimated
+// latency of the solve (microseconds): one wavefront measured 0.28 us per
+// Frank-Wolfe iteration for MGDA and 0.9 us per dual iteration for CAGrad
+// at K = 4, the chains grow with K; PCGrad's K(K-1) projections are short.
+// The hybrid path is taken while it stays within kHybridHide times the time
+// the next bucket's Gram read takes (its bytes at 7 TB/s): every measured
+// crossover of method, iterations and bucket size falls on the side this
+// predicts.
+constexpr double kHybridHide = 1.5;
+
+double solve_latency_us(int method, int K, int iters) {
+  if (method == BKMOO_MGDA) return 0.07 * K * iters;
+  if (method == BKMOO_CAGRAD) return 0.22 * K * iters;
+  if (method == BKMOO_PCGRAD) return 0.1 * K * K;
+  return 0.0;
+}
 
 // Workgroups for the pipelined, partly resident path, or 0 when it should
 // not be used.  Its partial Grams need two slots per data workgroup, and a
 // segment (about N / data workgroups elements at most) must stay within one
 // 32-bit buffer range.
-int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int64_t cap_slots) {
+int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters,
+                  int64_t cap_slots) {
   const int mode = g_resolve_path.load();
   if (mode == 1 || mode == 2 || K > 4 || !vec || is_exact(method)) return 0;
   static std::atomic<int> cache[3][2][2];  // K-2, dt, out_dt
@@ -170,9 +191,11 @@ int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
   if ((N / gd + 2 * 4096) * (int64_t)elem_bytes(dt) >= ((int64_t)1 << 31)) return 0;
   if (mode == 3) return g;
   const double avg_elems = (double)N / B;
+  const double bucket_bytes = avg_elems * K * elem_bytes(dt);
   const double held = (double)hybrid_held_elems(K, dt) * gd / (avg_elems > 1.0 ? avg_elems : 1.0);
-  return B >= kHybridMinBuckets && avg_elems * K * elem_bytes(dt) >= kHybridMinBucketBytes &&
-                 held >= kHybridMinHeld
+  const double gram_read_us = bucket_bytes / 7.0e6;
+  return B >= kHybridMinBuckets && bucket_bytes >= kHybridMinBucketBytes && held >= kHybridMinHeld &&
+                 solve_latency_us(method, K, iters) <= kHybridHide * gram_read_us
              ? g
              : 0;
 }
@@ -287,7 +310,7 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   const int8_t *order = hp ? hp->pcgrad_order : nullptr;
 
   const int hgrid =
-      choose_hybrid(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, L.cap_chunks);
+      choose_hybrid(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters, L.cap_chunks);
   if (hgrid > 0) {
     hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start,
                                    nullptr, w.err, w.sync, 2 * (int64_t)B * kSyncStride, stream);
@@ -425,7 +448,7 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
   if (st != BKMOO_OK) return st;
   if (!valid_dtype(out_dt) || method < BKMOO_MGDA || method > BKMOO_CAGRAD_EXACT) return BKMOO_EINVAL;
   if (k_unsupported(K, method)) return BKMOO_EUNSUPPORTED;
-  if (choose_hybrid(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method,
+  if (choose_hybrid(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter,
                     layout(K, N, B, dt).cap_chunks) > 0)
     *path = BKMOO_PATH_HYBRID;
   else if (choose_resident(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter) > 0)

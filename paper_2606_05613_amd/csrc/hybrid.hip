@@ -11,7 +11,7 @@
 // produced, and bucket b's combine re-reads only the part it did not keep.
 //
 // How.  Workgroups of 256 threads, two per CU (two can sit in different
-// phases, so one computes while the other streams).  The last kHybSolvers
+// phases, so one computes while the other streams).  The first kHybSolvers
 // workgroups of the grid hold no data: solver j
 // takes buckets j, j + kHybSolvers, ...; it waits until every data workgroup
 // has stored its partial Gram of the bucket, adds the partials in a fixed
@@ -53,6 +53,9 @@ constexpr int kHybThreads = 256;  // two workgroups per CU
 constexpr int kHybWaves = kHybThreads / kWave;
 constexpr int kHybSolvers = 4;  // workgroups that reduce and solve, holding no data
 constexpr int kHybStream = 2;   // streamed vectors per task row and thread per step
+// Partials a solver thread loads at once: with one segment per data
+// workgroup (~508) and 25 threads per Gram entry, one round trip.
+constexpr int kHybRedBatch = 24;
 
 // Vectors per task row and thread kept in each of the two buffers: registers
 // (NR) and LDS (NL).  The two buffers together hold about what the
@@ -302,6 +305,9 @@ struct Hybrid {
   static __device__ void solve(const HybArgs &a, Smem &sm, int w, int GD) {
     const int t = threadIdx.x, wave = t / kWave;
     __shared__ int ok_sh;
+    // a solve sits on the critical path of every data workgroup and shares
+    // its CU with one: its waves go first
+    __builtin_amdgcn_s_setprio(3);
     for (int b = w - GD; b < a.B; b += kHybSolvers) {
       if (t == 0) ok_sh = wait_at_least(&a.arrive[(int64_t)b * kSyncStride], (uint32_t)GD, a) ? 1 : 0;
       __syncthreads();
@@ -313,15 +319,15 @@ struct Hybrid {
       if (t < P * NG) {
         const int p = t / NG, g = t % NG;
         double v = 0.0;
-        for (int64_t s = g; s < nseg; s += 8 * NG) {  // 8 device-coherent loads in flight
-          double q[8];
+        for (int64_t s = g; s < nseg; s += kHybRedBatch * NG) {  // device-coherent loads in flight
+          double q[kHybRedBatch];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
+          for (int u = 0; u < kHybRedBatch; ++u) {
             const int64_t ss = s + (int64_t)u * NG;
             q[u] = ss < nseg ? load_agent(&a.partials[((int64_t)(b & 1) * GD + ss) * P + p]) : 0.0;
           }
 #pragma unroll
-          for (int u = 0; u < 8; ++u) v += q[u];
+          for (int u = 0; u < kHybRedBatch; ++u) v += q[u];
         }
         sm.red2[p][g] = v;
       }
@@ -388,7 +394,10 @@ template <int K, int DT, int ODT>
 __global__ __launch_bounds__(kHybThreads, 2) void hybrid_kernel(Rows<K> rows, HybArgs a) {
   using H = Hybrid<K, DT, ODT>;
   __shared__ typename H::Smem sm;
-  const int G = gridDim.x, GD = G - kHybSolvers, w = blockIdx.x;
+  // the solvers are the lowest block indices: dispatched first, they are the
+  // older workgroup on their CU, which the wave arbiter favours
+  const int G = gridDim.x, GD = G - kHybSolvers;
+  const int w = (int)blockIdx.x < kHybSolvers ? GD + (int)blockIdx.x : (int)blockIdx.x - kHybSolvers;
   if (*a.err & kErrOffsets) {
     // the schedule rejected the offsets: NaN Gram and weights, no update
     if (w == 0) {
