@@ -258,6 +258,10 @@ struct Hybrid {
       for (int i = 0; i < K; ++i) sm.wsh[i] = load_agent(&a.weights[(int64_t)b * K + i]);
     }
     __syncthreads();
+    // The two workgroups of a CU drift into different phases, and the wave
+    // arbiter favours the older one; the combine (whose end releases the
+    // next Gram phase and whose writes are the slowest traffic) goes first.
+    __builtin_amdgcn_s_setprio(1);
     float wv[K];
 #pragma unroll
     for (int i = 0; i < K; ++i) wv[i] = sm.wsh[i];
@@ -299,6 +303,7 @@ struct Hybrid {
         }
       }
     }
+    __builtin_amdgcn_s_setprio(0);
   }
 
   // Solver workgroup: buckets j, j + kHybSolvers, ... (j = w - GD).
