@@ -26,7 +26,10 @@
 // and fixed-order reductions as the streaming pass), stores it in the
 // segment's slot and arrives at the bucket's counter.  A combine phase waits
 // for the bucket's flag (bounded) and writes the update from the buffer and
-// from a second read of the streamed part.
+// from a second read of the streamed part.  The Gram phase reads the
+// streamed part with the temporal cache policy, so that second read mostly
+// hits the Infinity Cache; solver waves, and data waves in a combine phase,
+// run at raised wave priority.
 //
 // No cycle of waits: a data workgroup waits for bucket b's weights only after
 // it has arrived for bucket b+1, every data workgroup arrives for bucket b
