@@ -177,7 +177,7 @@ def main():
                  bkmoo.PATH_HYBRID: "hybrid"}[path]
     # the cooperative paths are one kernel: time the whole resolve call
     resident = path in (bkmoo.PATH_RESIDENT, bkmoo.PATH_HYBRID)
-    traffic_bytes = bkmoo.resolve_traffic(K, wl.offsets(), wl.dtype, path)
+    traffic_bytes = bkmoo.resolve_traffic(K, wl.offsets(), wl.dtype, path, method=wl.method, max_iter=wl.max_iter)
     log(f"resolve path: {path_name}; it requests {traffic_bytes / 1e9:.2f} GB from memory per step")
 
     def step(ev=None):

@@ -224,7 +224,9 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  *             about half of each bucket stays on chip between its Gram and
  *             its combine and the rest is read again (mostly from the
  *             last-level cache).  Same agreement with the two-pass path as
- *             the resident one; results depend on the device's CU count.
+ *             the resident one; results depend on the device's CU count and, for
+ *             K = 4 with MGDA or CAGrad, on the segment layout the method
+ *             selects (deterministic for given arguments).
  * The hybrid path is chosen first: for at least 8 buckets averaging at
  * least 48 MiB (all K rows) of which at least 10% stays on chip, and a
  * solve whose estimated latency (0.07 K us per MGDA iteration, 0.22 K us
@@ -324,13 +326,18 @@ bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *c
  *                        workgroup did not keep on chip (read twice)
  * with s, s_out the input and output element sizes.  The small per-bucket
  * terms (offsets, Gram matrices, weights, partial sums) are left out.  The
- * cooperative paths depend on the current device's CU count.  BKMOO_EINVAL
- * for bad sizes or pointers, invalid offsets or an unknown path;
+ * cooperative paths depend on the current device's CU count; the hybrid
+ * path's segments also on the method and iteration count (`method`,
+ * `max_iter`, as given to bkmoo_resolve), which decide whether the first
+ * workgroup of each CU takes a longer segment.  BKMOO_EINVAL
+ * for bad sizes or pointers, invalid offsets, method or iteration count, or
+ * an unknown path;
  * BKMOO_EUNSUPPORTED for a cooperative path with K > 4; BKMOO_EHIP when the
  * current device cannot be queried.
  */
 bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_t *offsets_host,
-                                   bkmoo_dtype dt, bkmoo_dtype out_dt, int32_t path, uint64_t *bytes);
+                                   bkmoo_dtype dt, bkmoo_dtype out_dt, bkmoo_method method, int32_t max_iter,
+                                   int32_t path, uint64_t *bytes);
 
 /*
  * bkmoo_read_device_error — copy the workspace's device error word into

@@ -52,7 +52,8 @@ def _load():
                           vp, ctypes.c_int, vp, vp, vp, vp, sz, vp],
         "bkmoo_conflicts": [i32, i32, vp, vp, vp, vp, vp],
         "bkmoo_slice_offsets": [i32, i32, vp, vp, vp],
-        "bkmoo_resolve_traffic": [i32, i64, i32, vp, ctypes.c_int, ctypes.c_int, i32, ctypes.POINTER(ctypes.c_uint64)],
+        "bkmoo_resolve_traffic": [i32, i64, i32, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, i32, i32,
+                                  ctypes.POINTER(ctypes.c_uint64)],
         "bkmoo_gram_reduce": [i32, i32, i32, vp, ctypes.c_int, vp, vp],
         "bkmoo_read_device_error": [vp, ctypes.POINTER(u32), vp],
         "bkmoo_set_grid_override": [i32],
@@ -320,7 +321,8 @@ def resolve_path(grads: Grads, bucket_offsets_len: int, method: str = "mgda", ma
     return out.value
 
 
-def resolve_traffic(K: int, bucket_offsets, dtype, path: int, out_dtype=None) -> int:
+def resolve_traffic(K: int, bucket_offsets, dtype, path: int, out_dtype=None, method: str = "mgda",
+                    max_iter: int = 20) -> int:
     """Bytes a resolve on `path` requests from memory for these offsets (a
     host int64 array-like of B+1 entries); on the hybrid path part of the
     re-read is served by the last-level cache."""
@@ -330,8 +332,8 @@ def resolve_traffic(K: int, bucket_offsets, dtype, path: int, out_dtype=None) ->
     dt = code(dtype)
     odt = dt if out_dtype is None else code(out_dtype)
     out = ctypes.c_uint64(0)
-    _check(_lib.bkmoo_resolve_traffic(K, int(offs[-1]), len(offs) - 1, offs.ctypes.data, dt, odt, int(path),
-                                      ctypes.byref(out)), "bkmoo_resolve_traffic")
+    _check(_lib.bkmoo_resolve_traffic(K, int(offs[-1]), len(offs) - 1, offs.ctypes.data, dt, odt, METHODS[method],
+                                      int(max_iter), int(path), ctypes.byref(out)), "bkmoo_resolve_traffic")
     return out.value
 
 

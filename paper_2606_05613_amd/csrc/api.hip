@@ -164,6 +164,32 @@ constexpr double kHybridMinHeld = 0.1;                      // fraction of a buc
 // predicts.
 constexpr double kHybridHide = 1.5;
 
+// Segment skew for the hybrid kernel (per mille; hybrid_segment).  The
+// workgroups dispatched second onto a CU lose the wave arbiter to the first
+// and arrive last at every bucket, so the first ones can take more data.
+// Measured on MI355X (one process, K=4 bf16): a 35% skew takes 25 MiB
+// buckets from 18.4 to 17.7 ms with MGDA FW-20 (27.4 -> 24.8 with FW-100)
+// and 16 MiB buckets 7% lower, but slows the mean method by 2-5%, 50 MiB
+// CAGrad by 5%, 100 MiB buckets by 2%, and K = 2 or 3 by 5-30% (their
+// second workgroups' segments would no longer fill what they keep on chip).
+constexpr int kHybridSkewPm = 350;
+constexpr double kHybridSkewMaxRowBytes = 32.0 * (1 << 20);
+
+int hybrid_skew_pm(int K, int dt, int method, int iters, int64_t N, int B, int grid) {
+  if (K != 4 || (method != BKMOO_MGDA && method != BKMOO_CAGRAD) || iters <= 0 || B <= 0) return 0;
+  const double avg = (double)N / B;
+  if (avg * elem_bytes(dt) > kHybridSkewMaxRowBytes) return 0;
+  const int gd = hybrid_data_workgroups(grid), older = hybrid_older_workgroups(grid);
+  if (older <= 0 || older >= gd) return 0;
+  // the second workgroups' segments must still fill their on-chip share
+  const int64_t unit = hybrid_unit_elems(dt), nb = hybrid_held_elems(K, dt) / unit;
+  const int64_t nu = (int64_t)(avg / unit);
+  const int64_t co = (nu * (1000 + kHybridSkewPm) + (int64_t)gd * 1000 - 1) / ((int64_t)gd * 1000);
+  const int64_t rest = nu - (int64_t)older * co;
+  const int64_t cy = rest > 0 ? (rest + (gd - older) - 1) / (gd - older) : 0;
+  return cy >= nb ? kHybridSkewPm : 0;
+}
+
 double solve_latency_us(int method, int K, int iters) {
   if (method == BKMOO_MGDA) return 0.07 * K * iters;
   if (method == BKMOO_CAGRAD) return 0.22 * K * iters;
@@ -317,7 +343,7 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
     if (e != hipSuccess) return BKMOO_EHIP;
     e = launch_hybrid(K, (int)dt, (int)out_dt, grads, bucket_offsets, B, shift, (int)method, iters, c,
                       order, G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride, w.err, g_spin_limit.load(),
-                      hgrid, stream);
+                      hgrid, hybrid_skew_pm(K, (int)dt, (int)method, iters, N, B, hgrid), stream);
     return hip_status(e);
   }
   const int rgrid = choose_resident(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters);
@@ -379,10 +405,12 @@ bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *c
 }
 
 bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_t *offsets_host,
-                                   bkmoo_dtype dt, bkmoo_dtype out_dt, int32_t path, uint64_t *bytes) {
+                                   bkmoo_dtype dt, bkmoo_dtype out_dt, bkmoo_method method, int32_t max_iter,
+                                   int32_t path, uint64_t *bytes) {
   bkmoo_status st = check_shape(K, N, B, dt);
   if (st != BKMOO_OK) return st;
   if (!offsets_host || !bytes || !valid_dtype(out_dt)) return BKMOO_EINVAL;
+  if (method < BKMOO_MGDA || method > BKMOO_CAGRAD_EXACT || max_iter < 0) return BKMOO_EINVAL;
   if (offsets_host[0] != 0 || offsets_host[B] != N) return BKMOO_EINVAL;
   for (int b = 0; b < B; ++b)
     if (offsets_host[b + 1] < offsets_host[b]) return BKMOO_EINVAL;
@@ -408,15 +436,16 @@ bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_
   } else {
     const int g = hybrid_grid(K, (int)dt, (int)out_dt);
     if (g <= 0) return BKMOO_EUNSUPPORTED;
-    const int gd = hybrid_data_workgroups(g);
+    const int gd = hybrid_data_workgroups(g), older = hybrid_older_workgroups(g);
+    const int skew = older > 0 ? hybrid_skew_pm(K, (int)dt, (int)method, max_iter, N, B, g) : 0;
     const int64_t unit = hybrid_unit_elems((int)dt), held = hybrid_held_elems(K, (int)dt);
     for (int b = 0; b < B; ++b) {  // each segment re-reads what it did not keep
       const int64_t n = offsets_host[b + 1] - offsets_host[b];
-      int64_t len = (n + gd - 1) / gd;
-      len = (len + unit - 1) / unit * unit;
-      for (int64_t lo = 0; len > 0 && lo < n; lo += len) {
-        const int64_t m = lo + len < n ? len : n - lo;
-        if (m > held) reread += (uint64_t)(m - held);
+      int64_t lo, hi, nseg, ns;
+      hybrid_segment(n, 0, gd, older, skew, unit, lo, hi, nseg);
+      for (int w = 0; w < nseg; ++w) {
+        hybrid_segment(n, w, gd, older, skew, unit, lo, hi, ns);
+        if (hi - lo > held) reread += (uint64_t)(hi - lo - held);
       }
     }
   }

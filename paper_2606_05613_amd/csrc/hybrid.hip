@@ -16,9 +16,11 @@
 // takes buckets j, j + kHybSolvers, ...; it waits until every data workgroup
 // has stored its partial Gram of the bucket, adds the partials in a fixed
 // order, solves on one wavefront and publishes the weights with a flag.  A
-// data workgroup w owns the w-th of at most GD equal segments of every bucket
+// data workgroup w owns the w-th of at most GD segments of every bucket
 // (GD data workgroups; segments are whole multiples of one vector per
-// thread).  Of its segment it keeps the first NB = NR + NL vectors per task
+// thread; equal, or longer for the workgroups dispatched first onto their
+// CU when the host asks for a skew, see hybrid_segment).  Of its segment it
+// keeps the first NB = NR + NL vectors per task
 // row and thread in one of two buffers (registers and LDS) and streams the
 // rest.  Per workgroup the order is
 //   Gram(0) -> A, Gram(1) -> B, Combine(0) <- A, Gram(2) -> A, Combine(1) <- B, ...
@@ -41,9 +43,9 @@
 // Cross-workgroup data moves through the agent-scope primitives of
 // coop_common.h.
 //
-// The segment length depends on the number of data workgroups, so results
-// are reproducible on a given device but may differ in the last bits between
-// devices with different CU counts (unlike the streaming passes).
+// The segments depend on the number of data workgroups (and on the skew), so
+// results are reproducible on a given device but may differ in the last bits
+// between devices with different CU counts (unlike the streaming passes).
 #include "combine_impl.h"
 #include "coop_common.h"
 #include "solve_impl.h"
@@ -82,6 +84,7 @@ struct HybArgs {
   uint32_t *flags;   // [B] at stride kSyncStride, zero at launch
   uint32_t *err;
   uint32_t spin_limit;
+  int older, skew_pm;  // segment layout (hybrid_segment)
 };
 
 // buf_load16 with the default (temporal) cache policy: the line may stay in
@@ -91,12 +94,6 @@ __device__ __forceinline__ u32x4 buf_load16_keep(Rsrc r, uint32_t voff, uint32_t
   return __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
 }
 
-// Segment length of bucket b: ceil(n_b / GD) rounded up to `unit` elements.
-__device__ __forceinline__ int64_t seg_len(const int64_t *offs, int b, int GD, int64_t unit) {
-  const int64_t n = offs[b + 1] - offs[b];
-  const int64_t len = (n + GD - 1) / GD;
-  return (len + unit - 1) / unit * unit;
-}
 
 // Bounded wait until *p reaches `target` (thread 0 only); on timeout the
 // error word gets kErrTimeout and false is returned.
@@ -135,10 +132,11 @@ struct Hybrid {
   static __device__ __forceinline__ void gram(const Rows<K> &rows, const HybArgs &a, Smem &sm, int b, int w, int GD,
                               int X, u32x4 (&reg)[NR][K], float (&hs)[K]) {
     const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
-    const int64_t len = seg_len(a.offs, b, GD, (int64_t)T * V);
-    const int64_t lo = a.offs[b] + (int64_t)w * len;
-    const int64_t hi = lo + len < a.offs[b + 1] ? lo + len : a.offs[b + 1];
-    const bool has = len > 0 && lo < hi;  // uniform over the workgroup
+    int64_t lo, hi, nseg;
+    hybrid_segment(a.offs[b + 1] - a.offs[b], w, GD, a.older, a.skew_pm, (int64_t)T * V, lo, hi, nseg);
+    lo += a.offs[b];
+    hi += a.offs[b];
+    const bool has = lo < hi;  // uniform over the workgroup
     float acc[P];
 #pragma unroll
     for (int p = 0; p < P; ++p) acc[p] = 0.0f;
@@ -268,10 +266,11 @@ struct Hybrid {
     float wv[K];
 #pragma unroll
     for (int i = 0; i < K; ++i) wv[i] = sm.wsh[i];
-    const int64_t len = seg_len(a.offs, b, GD, (int64_t)T * V);
-    const int64_t lo = a.offs[b] + (int64_t)w * len;
-    const int64_t hi = lo + len < a.offs[b + 1] ? lo + len : a.offs[b + 1];
-    if (len > 0 && lo < hi) {
+    int64_t lo, hi, nseg;
+    hybrid_segment(a.offs[b + 1] - a.offs[b], w, GD, a.older, a.skew_pm, (int64_t)T * V, lo, hi, nseg);
+    lo += a.offs[b];
+    hi += a.offs[b];
+    if (lo < hi) {
       const Split<V> sp(lo, hi, a.shift);
       if (t < sp.nh + sp.nt) {
         const int64_t n = t < sp.nh ? lo + t : sp.hi_a + (t - sp.nh);
@@ -319,9 +318,8 @@ struct Hybrid {
     for (int b = w - GD; b < a.B; b += kHybSolvers) {
       if (t == 0) ok_sh = wait_at_least(&a.arrive[(int64_t)b * kSyncStride], (uint32_t)GD, a) ? 1 : 0;
       __syncthreads();
-      const int64_t len = seg_len(a.offs, b, GD, (int64_t)T * V);
-      const int64_t n = a.offs[b + 1] - a.offs[b];
-      const int64_t nseg = len > 0 ? (n + len - 1) / len : 0;
+      int64_t slo, shi, nseg;
+      hybrid_segment(a.offs[b + 1] - a.offs[b], 0, GD, a.older, a.skew_pm, (int64_t)T * V, slo, shi, nseg);
       // segment slots in a fixed order: group g of entry p sums segments
       // g, g+NG, ... ascending, then entry p sums its groups ascending
       if (t < P * NG) {
@@ -473,6 +471,14 @@ int hybrid_grid(int K, int dt, int out_dt) {
 
 int hybrid_data_workgroups(int grid) { return grid - kHybSolvers; }
 
+// The dispatcher gives every CU one workgroup before it gives any a second,
+// so with two per CU the first (cu count - solvers) data workgroups are the
+// older resident of their CU.
+int hybrid_older_workgroups(int grid) {
+  const int cus = device_cu_count();
+  return grid == 2 * cus && cus > kHybSolvers ? cus - kHybSolvers : 0;
+}
+
 int64_t hybrid_held_elems(int K, int dt) {
   return (int64_t)kHybThreads * (hyb_regs(K) + hyb_lds(K)) * vec_elems(dt);
 }
@@ -482,9 +488,11 @@ int64_t hybrid_unit_elems(int dt) { return (int64_t)kHybThreads * vec_elems(dt);
 hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
                          int shift, int method, int iters, double c, const int8_t *order, double *gram,
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
-                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid, hipStream_t s) {
+                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid, int skew_pm,
+                         hipStream_t s) {
+  const int older = hybrid_older_workgroups(grid);
   const HybArgs a{offs, B, shift, method, iters, c, order, gram, weights, aux, out,
-                  partials, arrive, flags, err, spin_limit};
+                  partials, arrive, flags, err, spin_limit, older, older > 0 ? skew_pm : 0};
 #define BKMOO_HYB_CASE(k)                                                                        \
   case k:                                                                                        \
     if (dt == F32)                                                                               \

@@ -162,6 +162,38 @@ hipError_t launch_resident(int K, int dt, int out_dt, const void *const *rows, c
 // (the rest solve); partials must hold 2 * data workgroups slots.
 int hybrid_grid(int K, int dt, int out_dt);
 int hybrid_data_workgroups(int grid);
+// Data workgroups dispatched first onto their CU (0 unless the grid is two
+// workgroups per CU): the ones a segment skew gives more data.
+int hybrid_older_workgroups(int grid);
+
+// Segment [lo, hi) (relative to the bucket start) of data workgroup w in a
+// bucket of n elements, over gd data workgroups in whole units of `unit`
+// elements, and the number nseg of non-empty segments, which are always
+// workgroups 0 .. nseg-1.  skew_pm = 0: equal shares.  Otherwise the first
+// `older` workgroups take (1 + skew_pm/1000) times an equal share (rounded
+// up) and the others split the rest evenly.  Shared by the kernel and the
+// host's traffic count.
+__host__ __device__ inline void hybrid_segment(int64_t n, int w, int gd, int older, int skew_pm, int64_t unit,
+                                               int64_t &lo, int64_t &hi, int64_t &nseg) {
+  const int64_t nu = (n + unit - 1) / unit;
+  int64_t s, e;
+  if (skew_pm <= 0 || older <= 0 || older >= gd) {
+    const int64_t c = (nu + gd - 1) / gd;
+    s = (int64_t)w * c;
+    e = s + c;
+    nseg = c > 0 ? (nu + c - 1) / c : 0;
+  } else {
+    const int64_t co = (nu * (1000 + skew_pm) + (int64_t)gd * 1000 - 1) / ((int64_t)gd * 1000);
+    const int64_t rest = nu - (int64_t)older * co;
+    const int gy = gd - older;
+    const int64_t cy = rest > 0 ? (rest + gy - 1) / gy : 0;
+    s = w < older ? (int64_t)w * co : (int64_t)older * co + (int64_t)(w - older) * cy;
+    e = w < older ? s + co : s + cy;
+    nseg = co == 0 ? 0 : rest <= 0 ? (nu + co - 1) / co : older + (cy > 0 ? (rest + cy - 1) / cy : 0);
+  }
+  lo = s * unit < n ? s * unit : n;
+  hi = e * unit < n ? e * unit : n;
+}
 // Elements of its segment a data workgroup keeps on chip per bucket, and the
 // granule segment lengths are rounded up to.
 int64_t hybrid_held_elems(int K, int dt);
@@ -169,7 +201,8 @@ int64_t hybrid_unit_elems(int dt);
 hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
                          int shift, int method, int iters, double c, const int8_t *order, double *gram,
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
-                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid, hipStream_t s);
+                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid, int skew_pm,
+                         hipStream_t s);
 
 int device_cu_count();
 

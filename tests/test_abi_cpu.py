@@ -167,6 +167,12 @@ def test_resolve_traffic_two_pass_and_errors(b):
             b.resolve_traffic(4, np.array(bad), "bf16", b.PATH_TWO_PASS)
     with pytest.raises(b.BkmooError, match="EINVAL"):
         b.resolve_traffic(4, offs, "bf16", 7)
+    with pytest.raises(b.BkmooError, match="EINVAL"):
+        b.resolve_traffic(4, offs, "bf16", b.PATH_TWO_PASS, max_iter=-1)
+    L = b._lib
+    out = ctypes.c_uint64(0)
+    o = np.ascontiguousarray(offs, dtype=np.int64)
+    assert L.bkmoo_resolve_traffic(4, 40, 4, o.ctypes.data, 1, 1, 9, 20, b.PATH_TWO_PASS, ctypes.byref(out)) == -1
 
 
 def test_grid_override_rejects_negative(b):

@@ -75,6 +75,29 @@ def test_coop_full_size_buckets(coop):
     print(f"case path {path} 3 x 25 MiB", full_parity(lib, wl), flush=True)
 
 
+@pytest.mark.parametrize("method", ["cagrad", "mgda"])
+def test_hybrid_skewed_segments(gpu_lib, method):
+    """K=4 bf16 buckets of 9.5-16.8M elements with an MGDA or CAGrad solve:
+    the hybrid kernel gives the first workgroup of each CU a longer segment
+    (the traffic count differs from the even layout's), results match the
+    oracle and repeat bitwise."""
+    lens = [9_500_001, 13_107_200, 11_000_003, 16_777_216]
+    wl = small_workload(BASE, sum(lens), bucket_lens=lens, K=4, dtype="bf16", method=method, seed=630)
+    skewed = gpu_lib.resolve_traffic(4, wl.offsets(), "bf16", gpu_lib.PATH_HYBRID, method=method, max_iter=20)
+    even = gpu_lib.resolve_traffic(4, wl.offsets(), "bf16", gpu_lib.PATH_HYBRID, method="mean", max_iter=0)
+    assert skewed != even
+    grads, offs, order = to_device_inputs(wl)
+    gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
+    try:
+        print(f"case skewed hybrid {method}", full_parity(gpu_lib, wl, grads=grads), flush=True)
+        r1 = run_resolve(gpu_lib, wl, grads, offs, order)
+        r2 = run_resolve(gpu_lib, wl, grads, offs, order)
+    finally:
+        gpu_lib.set_resolve_path(0)
+    assert np.array_equal(r1["gram"], r2["gram"]) and np.array_equal(r1["weights"], r2["weights"])
+    assert torch.equal(r1["out"].view(torch.int16), r2["out"].view(torch.int16))
+
+
 def test_coop_bucket_larger_than_chip(coop):
     """One K=2 fp32 bucket of 14.5M elements: the resident kernel's
     workgroups hold several segments and re-read them; the hybrid kernel's
