@@ -85,13 +85,22 @@ def test_row_layouts(gpu_lib, dtype, layout):
     print(full_parity(gpu_lib, wl, grads=rows), flush=True)
 
 
-def test_in_place_update(gpu_lib):
-    wl = small_workload(BASE, 50_000, bucket_lens=[20_000, 30_000], K=4, dtype="bf16", seed=4)
+@pytest.mark.parametrize("path", ["PATH_TWO_PASS", "PATH_RESIDENT", "PATH_HYBRID"])
+def test_in_place_update(gpu_lib, path):
+    """The update written over one of the gradient rows equals the
+    out-of-place update of the same path bitwise (every position is read
+    before it is written, on each path)."""
+    wl = small_workload(BASE, 350_008, bucket_lens=[20_000, 130_000, 1, 200_007], K=4, dtype="bf16", seed=4)
     g = fill_grads(wl, device="cuda")
     offs = torch.from_numpy(wl.offsets()).cuda()
-    ref = gpu_lib.resolve(g.clone(), offs, wl.method, max_iter=wl.max_iter, cagrad_c=wl.cagrad_c)
-    gpu_lib.resolve(g, offs, wl.method, max_iter=wl.max_iter, cagrad_c=wl.cagrad_c, out=g[2])
-    torch.cuda.synchronize()
+    gpu_lib.set_resolve_path(getattr(gpu_lib, path))
+    try:
+        assert gpu_lib.resolve_path(g, wl.B + 1, wl.method, wl.max_iter) == getattr(gpu_lib, path)
+        ref = gpu_lib.resolve(g.clone(), offs, wl.method, max_iter=wl.max_iter, cagrad_c=wl.cagrad_c)
+        gpu_lib.resolve(g, offs, wl.method, max_iter=wl.max_iter, cagrad_c=wl.cagrad_c, out=g[2])
+        torch.cuda.synchronize()
+    finally:
+        gpu_lib.set_resolve_path(0)
     assert torch.equal(g[2].view(torch.int16), ref.view(torch.int16))
 
 
