@@ -5,8 +5,9 @@
 A step is one pass of the whole hot path over the workload's gradients,
 already resident in HBM: the per-bucket Gram matrices, the per-bucket solve
 and the combined update.  The step runs what bkmoo_resolve runs for the
-workload: the single-read resident kernel when it applies (one call), else
-the two-pass kernels through the three stage entry points in stream order
+workload: one of its cooperative kernels (the pipelined, partly resident
+one or the single-read one) when it takes one, as one call, else the
+two-pass kernels through the three stage entry points in stream order
 (identical results to bkmoo_resolve's two-pass path, and each stage can be
 timed).  The default workload is the Llama-3-8B-shaped K=4 bf16 MGDA
 (Frank-Wolfe, 20 iterations) case with 25 MiB buckets.  Prints ONE JSON
@@ -23,8 +24,10 @@ Reported next to the throughput:
                which the last-level cache serves.  `traffic` (HBM bytes per
                launch) comes from the committed rocprofv3 counter summary
                when it matches the current kernel source, else null;
+  two_pass     when the step ran a cooperative kernel: the plain two-pass
+               resolve on the same inputs, with its (2K+1)*s*N bytes;
   cpu_baseline the float64 oracle on a bounded prefix of the same buckets,
-               on this host's cores.
+               on this host's cores (count and model).
 """
 
 from __future__ import annotations
@@ -108,7 +111,13 @@ def cpu_baseline(wl, grads, target_s: float):
         spent += time.perf_counter() - t0
         done_elems += hi - lo
         nb += 1
-    return {"value": wl.K * done_elems / spent, "unit": "elem/s", "cores": int(cores), "kind": "oracle",
+    cpu = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            cpu = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
+    except OSError:
+        pass
+    return {"value": wl.K * done_elems / spent, "unit": "elem/s", "cores": int(cores), "cpu": cpu, "kind": "oracle",
             "sample": f"first {nb} of {wl.B} buckets ({wl.K}x{done_elems} elements), oracle.resolve "
                       f"end to end (Gram, {wl.method}, combine, rounding), {spent:.1f} s"}
 
@@ -226,6 +235,35 @@ def main():
             st["combine"] += ev[2].elapsed_time(ev[3]) / args.steps
     log(f"{ms_step:.3f} ms/step; stages (ms) " + ", ".join(f"{k} {v:.3f}" for k, v in st.items()))
 
+    # the plain two-pass resolve on the same inputs, reported beside a
+    # cooperative path's figure (whose re-reads may hit the last-level cache)
+    two_pass = None
+    if resident:
+        saved = {"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS, "resident": bkmoo.PATH_RESIDENT,
+                 "hybrid": bkmoo.PATH_HYBRID}[args.path]
+        bkmoo.set_resolve_path(bkmoo.PATH_TWO_PASS)
+        try:
+            def two_pass_step():
+                bkmoo.resolve(grads, offs, wl.method, wl.max_iter, wl.cagrad_c, pcgrad_order=order, out=out,
+                              gram_out=G, weights=W, aux=A, workspace=ws)
+            for _ in range(2):
+                two_pass_step()
+            e0t, e1t = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            reps = max(3, args.steps // 2)
+            e0t.record(stream)
+            for _ in range(reps):
+                two_pass_step()
+            e1t.record(stream)
+            torch.cuda.synchronize()
+        finally:
+            bkmoo.set_resolve_path(saved)
+        tp_ms = e0t.elapsed_time(e1t) / reps
+        tp_bytes = (2 * K + 1) * s * N
+        two_pass = {"ms_per_step": round(tp_ms, 4), "value": K * N / (tp_ms / 1e3),
+                    "algorithmic_bytes": tp_bytes, "GBps": round(tp_bytes / (tp_ms / 1e3) / 1e9, 1),
+                    "frac": round(tp_bytes / (tp_ms / 1e3) / 1e9 / PEAK_HBM_GBPS, 4)}
+        log(f"two-pass resolve on the same inputs: {tp_ms:.3f} ms/step ({two_pass['GBps']} GB/s)")
+
     # per-bucket conflict diagnostics on the step's Gram matrices: outside the
     # step (they read only the B*K*K Gram), timed on their own
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -324,6 +362,8 @@ def main():
         "resolve_requested_GBps": round(traffic_bytes / (ms_step / 1e3) / 1e9, 1),
         "roofline": roof,
     }
+    if two_pass is not None:
+        result["two_pass"] = two_pass
     if not args.no_cpu_baseline:
         log(f"oracle CPU baseline, ~{args.cpu_seconds:.0f} s")
         result["cpu_baseline"] = cpu_baseline(wl, grads, args.cpu_seconds)
