@@ -51,9 +51,11 @@ def test_coop_parity(coop, method, dtype, K):
 
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_coop_output_types(coop, out_dtype):
-    lib, _ = coop
+    lib, path = coop
     wl = small_workload(BASE, 200_000, bucket_lens=[99_999, 100_001], K=3, dtype="bf16", seed=77)
-    print(full_parity(lib, wl, out_dtype=out_dtype), flush=True)
+    grads, _, _ = to_device_inputs(wl)
+    assert lib.resolve_path(grads, wl.B + 1, wl.method, wl.max_iter, out_dtype=out_dtype) == path
+    print(full_parity(lib, wl, grads=grads, out_dtype=out_dtype), flush=True)
 
 
 @pytest.mark.parametrize("nb", [1, 2, 3, 41])
@@ -62,8 +64,11 @@ def test_coop_bucket_counts(coop, nb):
     lib, path = coop
     rng = np.random.default_rng(nb)
     lens = [int(x) for x in rng.integers(1, 90_000, size=nb)]
+    lens[-1] += -sum(lens) % 8  # rows of the [K, N] tensor at one 16-byte phase
     wl = small_workload(BASE, sum(lens), bucket_lens=lens, K=4, dtype="bf16", method="mgda", seed=600 + nb)
-    print(f"case path {path} B={nb}", full_parity(lib, wl), flush=True)
+    grads, _, _ = to_device_inputs(wl)
+    assert lib.resolve_path(grads, wl.B + 1, "mgda") == path
+    print(f"case path {path} B={nb}", full_parity(lib, wl, grads=grads), flush=True)
 
 
 def test_coop_full_size_buckets(coop):
@@ -72,39 +77,50 @@ def test_coop_full_size_buckets(coop):
     lib, path = coop
     wl = small_workload(BASE, 3 * 13_107_200, bucket_elems=13_107_200, K=4, dtype="bf16", method="mgda",
                         seed=620)
-    print(f"case path {path} 3 x 25 MiB", full_parity(lib, wl), flush=True)
+    grads, _, _ = to_device_inputs(wl)
+    assert lib.resolve_path(grads, wl.B + 1, "mgda") == path
+    print(f"case path {path} 3 x 25 MiB", full_parity(lib, wl, grads=grads), flush=True)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("method", ["cagrad", "mgda"])
-def test_hybrid_skewed_segments(gpu_lib, method):
-    """K=4 bf16 buckets of 9.5-16.8M elements with an MGDA or CAGrad solve:
-    the hybrid kernel gives the first workgroup of each CU a longer segment
-    (the traffic count differs from the even layout's), results match the
-    oracle and repeat bitwise."""
+def test_hybrid_skewed_segments(gpu_lib, method, dtype):
+    """K=4 buckets of 19-32 MiB per row (ragged) with an MGDA or CAGrad
+    solve: the hybrid kernel gives the first workgroup of each CU a longer
+    segment (the traffic count differs from the even layout's), results
+    match the oracle and repeat bitwise."""
     lens = [9_500_001, 13_107_200, 11_000_003, 16_777_216]
-    wl = small_workload(BASE, sum(lens), bucket_lens=lens, K=4, dtype="bf16", method=method, seed=630)
-    skewed = gpu_lib.resolve_traffic(4, wl.offsets(), "bf16", gpu_lib.PATH_HYBRID, method=method, max_iter=20)
-    even = gpu_lib.resolve_traffic(4, wl.offsets(), "bf16", gpu_lib.PATH_HYBRID, method="mean", max_iter=0)
+    if dtype == "f32":
+        lens = [n // 2 + 1 for n in lens]
+    lens[-1] += -sum(lens) % (8 if dtype == "bf16" else 4)  # rows at one 16-byte phase
+    wl = small_workload(BASE, sum(lens), bucket_lens=lens, K=4, dtype=dtype, method=method,
+                        seed=630 + (dtype == "f32"))
+    skewed = gpu_lib.resolve_traffic(4, wl.offsets(), dtype, gpu_lib.PATH_HYBRID, method=method, max_iter=20)
+    even = gpu_lib.resolve_traffic(4, wl.offsets(), dtype, gpu_lib.PATH_HYBRID, method="mean", max_iter=0)
     assert skewed != even
     grads, offs, order = to_device_inputs(wl)
     gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
     try:
+        assert gpu_lib.resolve_path(grads, wl.B + 1, method, 20) == gpu_lib.PATH_HYBRID
         print(f"case skewed hybrid {method}", full_parity(gpu_lib, wl, grads=grads), flush=True)
         r1 = run_resolve(gpu_lib, wl, grads, offs, order)
         r2 = run_resolve(gpu_lib, wl, grads, offs, order)
     finally:
         gpu_lib.set_resolve_path(0)
     assert np.array_equal(r1["gram"], r2["gram"]) and np.array_equal(r1["weights"], r2["weights"])
-    assert torch.equal(r1["out"].view(torch.int16), r2["out"].view(torch.int16))
+    assert torch.equal(r1["out"].view(torch.int32 if dtype == "f32" else torch.int16),
+                       r2["out"].view(torch.int32 if dtype == "f32" else torch.int16))
 
 
 def test_coop_bucket_larger_than_chip(coop):
     """One K=2 fp32 bucket of 14.5M elements: the resident kernel's
     workgroups hold several segments and re-read them; the hybrid kernel's
     segments stream most of their data."""
-    lib, _ = coop
+    lib, path = coop
     wl = small_workload(WORKLOADS["k2-mgda-1m-f32"], 14_500_000, bucket_lens=[14_500_000], seed=5)
-    print(full_parity(lib, wl), flush=True)
+    grads, _, _ = to_device_inputs(wl)
+    assert lib.resolve_path(grads, wl.B + 1, wl.method, wl.max_iter) == path
+    print(full_parity(lib, wl, grads=grads), flush=True)
 
 
 @pytest.mark.parametrize("path_name", ["PATH_RESIDENT", "PATH_HYBRID"])
@@ -113,6 +129,7 @@ def test_coop_deterministic_and_close_to_two_pass(gpu_lib, path_name):
     grads, offs, order = to_device_inputs(wl)
     try:
         gpu_lib.set_resolve_path(getattr(gpu_lib, path_name))
+        assert gpu_lib.resolve_path(grads, wl.B + 1, wl.method, wl.max_iter) == getattr(gpu_lib, path_name)
         r1 = run_resolve(gpu_lib, wl, grads, offs, order)
         r2 = run_resolve(gpu_lib, wl, grads, offs, order)
         gpu_lib.set_resolve_path(gpu_lib.PATH_TWO_PASS)
@@ -129,9 +146,10 @@ def test_coop_deterministic_and_close_to_two_pass(gpu_lib, path_name):
 def test_coop_wait_timeout_forced_from_host(coop):
     """A one-poll wait limit makes waiting workgroups give up at once: the
     call still completes (no hang) and, if any wait expired, says so."""
-    lib, _ = coop
+    lib, path = coop
     wl = small_workload(BASE, sum(LENS), bucket_lens=LENS, K=4, dtype="bf16", seed=41)
     grads, offs, _ = to_device_inputs(wl)
+    assert lib.resolve_path(grads, wl.B + 1, wl.method, wl.max_iter) == path
     ws = torch.empty(lib.workspace_size(wl.K, wl.N, wl.B, "bf16"), dtype=torch.uint8, device="cuda")
     try:
         lib.set_wait_limit(1)
