@@ -142,14 +142,20 @@ def _check_workload(lib, wl, grads, offs, order):
     print(f"  ok: buckets {picks} checked end to end", flush=True)
 
 
-@pytest.mark.parametrize("name", ["k2-mgda-1m-f32", "gpt2-124m-k4-pcgrad-f32", "llama3-8b-k4-mgda-bf16",
-                                  "llama3-8b-k8-cagrad-bf16"])
+# the path bkmoo_resolve takes for each workload (what bench.py times)
+EXPECTED_PATH = {"k2-mgda-1m-f32": "PATH_TWO_PASS", "gpt2-124m-k4-pcgrad-f32": "PATH_HYBRID",
+                 "llama3-8b-k4-mgda-bf16": "PATH_HYBRID", "llama3-8b-k8-cagrad-bf16": "PATH_TWO_PASS"}
+
+
+@pytest.mark.parametrize("name", list(EXPECTED_PATH))
 def test_full_workload(gpu_lib, name):
     _free()
     wl = WORKLOADS[name]
     grads = fill_grads(wl, device="cuda")
     offs = torch.from_numpy(wl.offsets()).cuda()
     order = torch.from_numpy(wl.orders()).cuda() if wl.method == "pcgrad" else None
+    gpu_lib.set_resolve_path(0)
+    assert gpu_lib.resolve_path(grads, wl.B + 1, wl.method, wl.max_iter) == getattr(gpu_lib, EXPECTED_PATH[name])
     try:
         _check_workload(gpu_lib, wl, grads, offs, order)
     finally:
