@@ -209,37 +209,33 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  * synchronisation.  gram, weights and aux may be NULL, in which case the
  * intermediate values live in the workspace only.
  *
- * Two implementations, same definitions and tolerances:
+ * Three implementations, same definitions and tolerances:
  *   two-pass  the kernels of bkmoo_gram, bkmoo_solve and bkmoo_combine;
  *             results equal those three calls bitwise.
- *   resident  (K <= 4, 16-byte-phase-aligned rows and output) one
- *             cooperative kernel keeps each bucket in registers and LDS
- *             between its Gram and its combine, so every gradient element
- *             is read from HBM once; the Gram sums run in a different (also
- *             fixed, grid-independent) order, so results agree with the
- *             two-pass path to rounding, not bitwise.  A bucket larger than
- *             the chip holds is read twice, still correct.
- *   hybrid    (K <= 4, aligned as above) one cooperative kernel in which
- *             the Gram pass of bucket b+1 runs while bucket b is solved;
- *             about half of each bucket stays on chip between its Gram and
- *             its combine and the rest is read again (mostly from the
- *             last-level cache).  Same agreement with the two-pass path as
- *             the resident one; results depend on the device's CU count and, for
- *             K = 4 with MGDA or CAGrad, on the segment layout the method
- *             selects (deterministic for given arguments).
- * The hybrid path is chosen first: for at least 8 buckets averaging at
- * least 48 MiB (all K rows) of which at least 10% stays on chip, and a
- * solve whose estimated latency (0.07 K us per MGDA iteration, 0.22 K us
- * per CAGrad iteration, 0.1 K^2 us for PCGrad, 0 for the mean) is at most
- * 1.5 times the time the next bucket's Gram read takes at 7 TB/s, so
- * that it hides behind it.  Exact solvers never take a cooperative path.
- * Else the resident path is chosen when the call has at least 32 buckets, the
- * average bucket holds at least 32 MiB of gradients and fits on chip, and
- * the solve is short (PCGrad, mean, or at most 2 Frank-Wolfe iterations):
- * each bucket's solve lies on the resident kernel's critical path, and the
- * cooperative launch costs more per call than the streaming passes, which
- * stay faster up to about 16-24 buckets.  bkmoo_resolve_path reports the choice;
- * bkmoo_set_resolve_path forces one.
+ *   hybrid    (K <= 4, 16-byte-phase-aligned rows and output) one
+ *             cooperative kernel in which the Gram pass of bucket b+1 runs
+ *             while bucket b is solved; about half of each bucket stays on
+ *             chip between its Gram and its combine and the rest is read
+ *             again (mostly from the last-level cache).  The Gram sums run
+ *             in a different (also fixed) order, so results agree with the
+ *             two-pass path to rounding, not bitwise; they depend on the
+ *             device's CU count and, for K = 4 with MGDA or CAGrad, on the
+ *             segment layout the method selects (deterministic for given
+ *             arguments).
+ *   resident  (K <= 4, aligned as above) one cooperative kernel keeps each
+ *             bucket in registers and LDS between its Gram and its combine,
+ *             so every gradient element is read from HBM once (a bucket
+ *             larger than the chip holds is read twice, still correct);
+ *             same agreement with the two-pass path.
+ * Automatic choice: the hybrid path for at least 8 buckets of which at
+ * least 10% stays on chip, averaging (all K rows) at least 24 MiB plus
+ * 4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA
+ * iteration, 0.22 K us per CAGrad iteration, 0.1 K^2 us for PCGrad, 0 for
+ * the mean), so that each bucket's hand-off is amortised; else the two
+ * passes.  Exact solvers never take a cooperative path.  The resident
+ * kernel runs only when forced: wherever it can run the hybrid kernel is
+ * faster, and below the hybrid's sizes so are the two passes.
+ * bkmoo_resolve_path reports the choice; bkmoo_set_resolve_path forces one.
  */
 bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
                            const int64_t *bucket_offsets, bkmoo_method method,
@@ -369,14 +365,15 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
  * bkmoo_set_resolve_path — force bkmoo_resolve's implementation
  * (0: automatic, BKMOO_PATH_TWO_PASS, BKMOO_PATH_RESIDENT or
  * BKMOO_PATH_HYBRID when eligible: K <= 4, aligned rows, not an exact
- * method; the hybrid path is taken only when forced).  Process-wide; for
+ * method; the resident path is taken only when forced).  Process-wide; for
  * tests and tuning.
  */
 bkmoo_status bkmoo_set_resolve_path(int32_t path);
 
 /*
- * bkmoo_set_wait_limit — polls of the resident path's bounded wait for a
- * bucket's weights before it gives up and sets BKMOO_DEVERR_TIMEOUT
+ * bkmoo_set_wait_limit — polls of the cooperative paths' bounded waits (for
+ * a bucket's arrivals or weights) before a workgroup gives up and sets
+ * BKMOO_DEVERR_TIMEOUT
  * (default 4194304, about a second or more).  Process-wide; lets tests force
  * the timeout path from the host.  0 is rejected.
  */

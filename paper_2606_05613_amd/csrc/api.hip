@@ -13,21 +13,16 @@ namespace {
 
 std::atomic<int> g_grid_override{0};
 std::atomic<int> g_resolve_path{0};            // 0 automatic, 1 two-pass, 2 resident, 3 hybrid
-std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the resident path's bounded wait
+std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the cooperative paths' bounded waits
 
-// Resident single-read resolve pays when a bucket is large enough to
-// amortise its grid-wide barrier, small enough to stay on chip, and its
-// solve is short: the solve of each bucket sits on the kernel's critical
-// path (a 20-iteration Frank-Wolfe costs about 7 us per bucket there, more
-// than the second read it saves on 25 MiB buckets), so iterative solvers
-// stay on the two-pass path unless they run at most kResidentMaxIters.  The
-// cooperative kernel also costs a few tens of microseconds per call more
-// than the streaming passes (measured on 25 MiB K=4 buckets: two-pass ahead
-// up to 8 buckets per call, resident ahead from about 16 (mean) or 24
-// (PCGrad)), so small calls stay on the two-pass path too.
-constexpr double kResidentMinBucketBytes = 32.0 * (1 << 20);
-constexpr int kResidentMaxIters = 2;
-constexpr int kResidentMinBuckets = 32;
+// The single-read (resident) kernel is never the automatic choice: wherever
+// it can run, the pipelined kernel can too and is faster, and at the bucket
+// sizes the pipelined kernel leaves to the two passes the resident one is
+// slower still.  Measured on MI355X, bf16, mean / PCGrad: 48 buckets of
+// 10.7 MiB per row (K=4) two-pass 1.00 ms, resident 1.51-1.58, pipelined
+// 0.70-0.72; 32 x 16 MiB (K=2) 0.50 / 1.09 / 0.40; 477 x 8 MiB (K=4) 7.1 /
+// 14.2 / 5.9; at 25 MiB (K=4, 613 buckets) 24.8 / 21.8 / 17.8.  It runs when
+// forced (bkmoo_set_resolve_path).
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cu_count[kMaxDevices];
@@ -120,49 +115,41 @@ Carved carve(void *ws, const Layout &L) {
                 reinterpret_cast<double *>(base + L.groups), reinterpret_cast<uint32_t *>(base + L.sync)};
 }
 
-// Workgroups for the resident path, or 0 when it should not be used.
+// Workgroups for the resident path when it is forced, else 0.
 int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters) {
-  const int mode = g_resolve_path.load();
-  if (mode == 1 || mode == 3 || K > 4 || !vec || is_exact(method)) return 0;
+  (void)N, (void)B, (void)iters;
+  if (g_resolve_path.load() != 2 || K > 4 || !vec || is_exact(method)) return 0;
   static std::atomic<int> cache[3][2][2];  // K-2, dt, out_dt (device model is fixed per process here)
   int g = cache[K - 2][dt][out_dt].load();
   if (g == 0) {
     g = resident_grid(K, dt, out_dt);
     cache[K - 2][dt][out_dt].store(g > 0 ? g : -1);
   }
-  if (g <= 0) return 0;
-  if (mode == 2) return g;
-  const double avg_elems = (double)N / B;
-  const double bucket_bytes = avg_elems * K * elem_bytes(dt);
-  const double fits = (double)resident_segment_elems(K, dt) * g;
-  const bool cheap_solve = method == BKMOO_PCGRAD || method == BKMOO_MEAN || iters <= kResidentMaxIters;
-  return B >= kResidentMinBuckets && bucket_bytes >= kResidentMinBucketBytes && avg_elems <= fits &&
-                 cheap_solve
-             ? g
-             : 0;
+  return g > 0 ? g : 0;
 }
 
 // The pipelined, partly resident path pays when each bucket carries enough
-// data to cover the latency of its solve and weight hand-off and a fair
-// share of each segment stays on chip.  Measured on MI355X (K = 2..4 bf16,
-// 2G elements, MGDA FW-20): buckets of 8 MiB per task run 22% slower than
-// the two streaming passes, 12 MiB ones tie, 16-50 MiB ones are 11-21%
-// faster, 100 MiB ones (12% kept on chip) 4% faster, and 200 or 400 MiB
-// ones (6-8% kept) 3-9% slower.
+// data to amortise its hand-off (reduction, solve, weights) and a fair
+// share of each segment stays on chip.  A bucket's solve runs on one
+// wavefront while the data workgroups stream the next bucket; its estimated
+// latency L (solve_latency_us) raises the bucket size needed:
+//   all K rows of the average bucket >= 24 MiB + 4 MiB per us of L,
+// at least 8 buckets, at least 10% of a bucket kept on chip.  Every
+// crossover measured on MI355X (K = 2..4 bf16, buckets of 4-400 MiB per
+// row, mean, PCGrad, MGDA and CAGrad with 20 or 100 iterations) falls on
+// the side this predicts or is a near-tie, except some K = 2 wins left to
+// the two passes (the K = 2 solves run faster than L assumes): for the mean
+// method the
+// two passes win at 16-20 MiB (all rows) and lose from 28 MiB (K=4: 5%
+// slower at 24 MiB, 12% faster at 28); MGDA FW-20 at K=4 (L = 5.6 us)
+// loses at 32 MiB, ties at 48 and wins 11-21% from 64; CAGrad FW-20 (L =
+// 17.6 us) loses at 64 MiB and wins at 100; MGDA FW-100 (L = 28 us) ties at
+// 100 MiB and wins at 200; buckets above ~150 MiB per row keep less than 10%
+// on chip and lose.
 constexpr int kHybridMinBuckets = 8;
-constexpr double kHybridMinBucketBytes = 48.0 * (1 << 20);  // all K rows
-constexpr double kHybridMinHeld = 0.1;                      // fraction of a bucket kept on chip
-
-// A bucket's solve runs on one wavefront while the data workgroups stream
-// the next bucket; what it cannot hide stalls every workgroup.  Estimated
-// latency of the solve (microseconds): one wavefront measured 0.28 us per
-// Frank-Wolfe iteration for MGDA and 0.9 us per dual iteration for CAGrad
-// at K = 4, the chains grow with K; PCGrad's K(K-1) projections are short.
-// The hybrid path is taken while it stays within kHybridHide times the time
-// the next bucket's Gram read takes (its bytes at 7 TB/s): every measured
-// crossover of method, iterations and bucket size falls on the side this
-// predicts.
-constexpr double kHybridHide = 1.5;
+constexpr double kHybridBaseMiB = 24.0;   // all K rows, no solve
+constexpr double kHybridMiBPerUs = 4.0;   // per microsecond of solve latency
+constexpr double kHybridMinHeld = 0.1;    // fraction of a bucket kept on chip
 
 // Segment skew for the hybrid kernel (per mille; hybrid_segment).  The
 // workgroups dispatched second onto a CU lose the wave arbiter to the first
@@ -190,6 +177,10 @@ int hybrid_skew_pm(int K, int dt, int method, int iters, int64_t N, int B, int g
   return cy >= nb ? kHybridSkewPm : 0;
 }
 
+// Estimated latency of one bucket's solve on one wavefront (microseconds):
+// 0.28 us per Frank-Wolfe iteration for MGDA and 0.9 us per dual iteration
+// for CAGrad measured at K = 4, chains growing with K; PCGrad's K(K-1)
+// projections are short.
 double solve_latency_us(int method, int K, int iters) {
   if (method == BKMOO_MGDA) return 0.07 * K * iters;
   if (method == BKMOO_CAGRAD) return 0.22 * K * iters;
@@ -219,11 +210,8 @@ int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
   const double avg_elems = (double)N / B;
   const double bucket_bytes = avg_elems * K * elem_bytes(dt);
   const double held = (double)hybrid_held_elems(K, dt) * gd / (avg_elems > 1.0 ? avg_elems : 1.0);
-  const double gram_read_us = bucket_bytes / 7.0e6;
-  return B >= kHybridMinBuckets && bucket_bytes >= kHybridMinBucketBytes && held >= kHybridMinHeld &&
-                 solve_latency_us(method, K, iters) <= kHybridHide * gram_read_us
-             ? g
-             : 0;
+  const double min_bytes = (kHybridBaseMiB + kHybridMiBPerUs * solve_latency_us(method, K, iters)) * (1 << 20);
+  return B >= kHybridMinBuckets && bucket_bytes >= min_bytes && held >= kHybridMinHeld ? g : 0;
 }
 
 }  // namespace

@@ -1,10 +1,11 @@
 """The automatic choice between the resolve paths (bkmoo_resolve_path) on
-MI355X shapes: the hybrid path needs at least 8 buckets of at least 48 MiB
-(all K rows), at least 10% of each kept on chip, and a solve short enough
-to hide behind the next bucket's Gram read; the resident path needs at
-least 32 buckets and a short solve; everything else runs the two passes.
-Only shapes are used (no resolve runs); the cases sit away from the
-thresholds."""
+MI355X shapes: the hybrid path needs at least 8 buckets, at least 10% of a
+bucket kept on chip, and buckets (all K rows) of at least 24 MiB plus
+4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA and
+0.22 K us per CAGrad iteration, 0.1 K^2 us for PCGrad); everything else
+runs the two passes.  The single-read resident kernel runs only when
+forced.  Only shapes are used (no resolve runs); the cases sit away from
+the thresholds."""
 
 import pytest
 import torch
@@ -20,20 +21,23 @@ def rows_4x2g():
     return torch.empty((4, 1 << 28), dtype=torch.bfloat16, device="cuda")
 
 
-# (buckets, method, iterations, expected path name)
+# (buckets, method, iterations, expected path name); rows of 512 MiB
 CASES_4x2G = [
-    (8, "mgda", 20, "hybrid"),      # 64 MiB per row: the solve hides (5.6 us vs 57 us)
-    (8, "mgda", 100, "hybrid"),     # 28 us
-    (8, "cagrad", 20, "hybrid"),    # 17.6 us
-    (8, "cagrad", 100, "two-pass"),  # 88 us: exposed
+    (8, "mgda", 20, "hybrid"),       # 256 MiB buckets (all rows) >= 24 + 4 * 5.6
+    (8, "mgda", 100, "hybrid"),      # >= 24 + 4 * 28
+    (8, "cagrad", 20, "hybrid"),     # >= 24 + 4 * 17.6
+    (8, "cagrad", 100, "two-pass"),  # < 24 + 4 * 88
     (8, "pcgrad", 0, "hybrid"),
     (8, "mean", 0, "hybrid"),
-    (32, "mgda", 20, "hybrid"),     # 16 MiB per row: 5.6 us vs 14.4 us
-    (32, "mgda", 100, "two-pass"),  # 28 us
-    (32, "cagrad", 20, "two-pass"),  # 17.6 us
-    (48, "mgda", 20, "two-pass"),   # 10.7 MiB per row: below 48 MiB all rows
-    (48, "mean", 0, "resident"),    # short solve, 48 buckets of 42.7 MiB
-    (4, "mean", 0, "two-pass"),     # fewer than 8 buckets
+    (32, "mgda", 20, "hybrid"),      # 64 MiB
+    (32, "mgda", 100, "two-pass"),
+    (32, "cagrad", 20, "two-pass"),
+    (48, "mgda", 20, "two-pass"),    # 42.7 MiB < 46.4
+    (48, "mean", 0, "hybrid"),
+    (64, "mean", 0, "hybrid"),       # 32 MiB
+    (64, "mgda", 20, "two-pass"),
+    (96, "mean", 0, "two-pass"),     # 21.3 MiB < 24
+    (4, "mean", 0, "two-pass"),      # fewer than 8 buckets
     (8, "mgda-exact", 0, "two-pass"),
 ]
 
@@ -62,3 +66,18 @@ def test_misaligned_rows_take_the_two_passes(gpu_lib):
     rows[1] = base[2 + (1 << 26): 2 + 2 * (1 << 26)]
     gpu_lib.set_resolve_path(0)
     assert gpu_lib.resolve_path(rows, 9, "mean", 0) == gpu_lib.PATH_TWO_PASS
+
+
+def test_resident_only_when_forced(gpu_lib, rows_4x2g):
+    """No shape makes the automatic choice the resident kernel; forced, it
+    runs wherever it can (aligned rows, K <= 4, iterative or not)."""
+    gpu_lib.set_resolve_path(0)
+    for B in (8, 32, 48, 64, 96, 613):
+        for m, it in (("mean", 0), ("pcgrad", 0), ("mgda", 2), ("mgda", 20)):
+            assert gpu_lib.resolve_path(rows_4x2g, B + 1, m, it) != gpu_lib.PATH_RESIDENT
+    gpu_lib.set_resolve_path(gpu_lib.PATH_RESIDENT)
+    try:
+        for B in (4, 48, 613):
+            assert gpu_lib.resolve_path(rows_4x2g, B + 1, "mgda", 20) == gpu_lib.PATH_RESIDENT
+    finally:
+        gpu_lib.set_resolve_path(0)
