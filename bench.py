@@ -185,12 +185,12 @@ def main():
     path_name = {bkmoo.PATH_TWO_PASS: "two-pass", bkmoo.PATH_RESIDENT: "resident",
                  bkmoo.PATH_HYBRID: "hybrid"}[path]
     # the cooperative paths are one kernel: time the whole resolve call
-    resident = path in (bkmoo.PATH_RESIDENT, bkmoo.PATH_HYBRID)
+    cooperative = path in (bkmoo.PATH_RESIDENT, bkmoo.PATH_HYBRID)
     traffic_bytes = bkmoo.resolve_traffic(K, wl.offsets(), wl.dtype, path, method=wl.method, max_iter=wl.max_iter)
     log(f"resolve path: {path_name}; it requests {traffic_bytes / 1e9:.2f} GB from memory per step")
 
     def step(ev=None):
-        if resident:
+        if cooperative:
             if ev is not None:
                 ev[0].record(stream)
             bkmoo.resolve(grads, offs, wl.method, wl.max_iter, wl.cagrad_c, pcgrad_order=order, out=out,
@@ -225,7 +225,7 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_start
     ms_step = t_wall * 1e3 / args.steps
-    if resident:
+    if cooperative:
         st = {"resolve": sum(ev[0].elapsed_time(ev[3]) for ev in events) / args.steps}
     else:
         st = {"gram": 0.0, "solve": 0.0, "combine": 0.0}
@@ -238,7 +238,7 @@ def main():
     # the plain two-pass resolve on the same inputs, reported beside a
     # cooperative path's figure (whose re-reads may hit the last-level cache)
     two_pass = None
-    if resident:
+    if cooperative:
         saved = {"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS, "resident": bkmoo.PATH_RESIDENT,
                  "hybrid": bkmoo.PATH_HYBRID}[args.path]
         bkmoo.set_resolve_path(bkmoo.PATH_TWO_PASS)
@@ -329,7 +329,7 @@ def main():
     # dominant kernel: the cooperative kernel (credited with the one-read
     # floor: the gradients once and the update), or the longer of the two
     # streaming passes
-    if resident:
+    if cooperative:
         kname, kbytes, kms = path_name, (K + 1) * s * N, st["resolve"]
     elif st["combine"] >= st["gram"]:
         kname, kbytes, kms = "combine", (K + 1) * s * N, st["combine"]
