@@ -94,7 +94,6 @@ __device__ __forceinline__ u32x4 buf_load16_keep(Rsrc r, uint32_t voff, uint32_t
   return __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
 }
 
-
 // Bounded wait until *p reaches `target` (thread 0 only); on timeout the
 // error word gets kErrTimeout and false is returned.
 __device__ bool wait_at_least(const uint32_t *p, uint32_t target, const HybArgs &a) {
