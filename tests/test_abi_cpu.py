@@ -38,6 +38,19 @@ def test_library_exports_every_declared_symbol(b):
     assert set(declared_functions()) <= set(b.EXPORTS)
 
 
+def test_binding_argument_counts_match_the_header(b):
+    """Every function the binding types has the header's number of
+    parameters (a signature change in one and not the other would pass
+    pointers in the wrong slots)."""
+    text = open(HEADER).read()
+    decls = re.findall(r"^(?:bkmoo_status|const char\s*\*)\s*(bkmoo_\w+)\s*\(([^;]*)\);", text, re.M)
+    assert decls and {n for n, _ in decls} == set(declared_functions())
+    for name, params in decls:
+        n_header = len([p for p in params.split(",") if p.strip()])
+        fn = getattr(b._lib, name)
+        assert fn.argtypes is not None and len(fn.argtypes) == n_header, name
+
+
 def test_status_strings(b):
     for code, word in ((0, "OK"), (-1, "EINVAL"), (-2, "EUNSUPPORTED"), (-3, "EWORKSPACE"), (-4, "EHIP")):
         assert word in b.status_string(code)
