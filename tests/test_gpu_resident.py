@@ -71,6 +71,19 @@ def test_coop_bucket_counts(coop, nb):
     print(f"case path {path} B={nb}", full_parity(lib, wl, grads=grads), flush=True)
 
 
+def test_coop_many_small_buckets(coop):
+    """1,500 ragged buckets of 1..2,000 elements (per-bucket counters and
+    flags for every bucket, most segments empty)."""
+    lib, path = coop
+    rng = np.random.default_rng(1500)
+    lens = [int(x) for x in rng.integers(1, 2_000, size=1500)]
+    lens[-1] += -sum(lens) % 8
+    wl = small_workload(BASE, sum(lens), bucket_lens=lens, K=4, dtype="bf16", method="cagrad", seed=1501)
+    grads, _, _ = to_device_inputs(wl)
+    assert lib.resolve_path(grads, wl.B + 1, "cagrad") == path
+    print(f"case path {path} B=1500", full_parity(lib, wl, grads=grads), flush=True)
+
+
 def test_coop_full_size_buckets(coop):
     """Three 25 MiB-per-task K=4 bf16 buckets: the hybrid kernel keeps part
     of each segment and streams the rest twice."""
