@@ -7,7 +7,9 @@ raises on any non-OK status.  There is no fallback: if the library is not
 built, importing this module fails.
 
 Names mirror include/bkmoo.h: workspace_size, gram, solve, combine, resolve,
-read_device_error, set_grid_override, status_string.
+conflicts, slice_offsets, gram_reduce, resolve_path, resolve_traffic,
+read_device_error, set_resolve_path, set_wait_limit, set_grid_override,
+status_string.
 """
 
 from __future__ import annotations
