@@ -4,8 +4,10 @@
 
 Every translation unit under csrc/ is compiled in parallel into _build/ and
 linked into paper_2606_05613_amd/libbkmoo.so.  All device code is built with
-packed-fp32 instruction selection disabled; the solver additionally without
-floating-point contraction so its scalar expressions round as written.
+packed-fp32 instruction selection disabled; the units holding the solvers
+(the solve and exact-solve kernels and the two cooperative kernels that
+embed them) and the conflict statistics additionally without floating-point
+contraction, so their scalar expressions round as written.
 
 After compiling, the generated gfx950 assembly is checked for a vector-memory
 store of more than 64 bits whose data registers an immediately following
