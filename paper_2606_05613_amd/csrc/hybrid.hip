@@ -57,7 +57,7 @@ namespace {
 constexpr int kHybThreads = 256;  // two workgroups per CU
 constexpr int kHybWaves = kHybThreads / kWave;
 constexpr int kHybSolvers = 4;  // workgroups that reduce and solve, holding no data
-constexpr int kHybStream = 2;   // streamed vectors per task row and thread per step
+constexpr int kHybStream = 2;   // streamed vectors per task row and thread per Gram-phase step
 // Partials a solver thread loads at once: with one segment per data
 // workgroup (~508) and 25 threads per Gram entry, one round trip.
 constexpr int kHybRedBatch = 24;
@@ -252,6 +252,25 @@ struct Hybrid {
   static __device__ __forceinline__ void combine(const Rows<K> &rows, const HybArgs &a, Smem &sm, int b, int w, int GD,
                                  int X, const u32x4 (&reg)[NR][K], const float (&hs)[K]) {
     const int t = threadIdx.x;
+    int64_t lo, hi, nseg;
+    hybrid_segment(a.offs[b + 1] - a.offs[b], w, GD, a.older, a.skew_pm, (int64_t)T * V, lo, hi, nseg);
+    lo += a.offs[b];
+    hi += a.offs[b];
+    const bool has = lo < hi;
+    const Split<V> sp(lo, has ? hi : lo, a.shift);
+    Rsrc rs[K];
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+      rs[i] = make_rsrc(static_cast<const char *>(rows.p[i]) + sp.lo_a * EB, (uint32_t)sp.nv * 16u);
+    const uint32_t voff = (uint32_t)t * 16u;
+    const int nslot = (sp.nv + T - 1) / T;
+    // The first re-read vector does not depend on the weights: loading it
+    // before the wait for them takes its latency off the combine, and the
+    // loop below keeps one vector per row in flight ahead of the one it
+    // combines (loads past the segment read zeros and are not used).
+    u32x4 qn[K];
+#pragma unroll
+    for (int i = 0; i < K; ++i) qn[i] = buf_load16(rs[i], voff, (uint32_t)(NB * T * 16));
     if (t == 0) {
       wait_at_least(&a.flags[(int64_t)b * kSyncStride], 1u, a);
 #pragma unroll
@@ -265,21 +284,11 @@ struct Hybrid {
     float wv[K];
 #pragma unroll
     for (int i = 0; i < K; ++i) wv[i] = sm.wsh[i];
-    int64_t lo, hi, nseg;
-    hybrid_segment(a.offs[b + 1] - a.offs[b], w, GD, a.older, a.skew_pm, (int64_t)T * V, lo, hi, nseg);
-    lo += a.offs[b];
-    hi += a.offs[b];
-    if (lo < hi) {
-      const Split<V> sp(lo, hi, a.shift);
+    if (has) {
       if (t < sp.nh + sp.nt) {
         const int64_t n = t < sp.nh ? lo + t : sp.hi_a + (t - sp.nh);
         store_elem<ODT>(a.out, n, wsum<K, ODT>(wv, hs));
       }
-      Rsrc rs[K];
-#pragma unroll
-      for (int i = 0; i < K; ++i)
-        rs[i] = make_rsrc(static_cast<const char *>(rows.p[i]) + sp.lo_a * EB, (uint32_t)sp.nv * 16u);
-      const uint32_t voff = (uint32_t)t * 16u;
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         u32x4 q[K];
@@ -289,19 +298,14 @@ struct Hybrid {
         combine_vec(wv, q, a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
       }
       // the re-read is the data's last use: streaming policy
-      const int nslot = (sp.nv + T - 1) / T;
-      for (int j0 = NB; j0 < nslot; j0 += kHybStream) {
-        u32x4 q[kHybStream][K];
+      for (int j0 = NB; j0 < nslot; ++j0) {
+        u32x4 q[K];
 #pragma unroll
-        for (int u = 0; u < kHybStream; ++u) {
+        for (int i = 0; i < K; ++i) q[i] = qn[i];
 #pragma unroll
-          for (int i = 0; i < K; ++i) q[u][i] = buf_load16(rs[i], voff, (uint32_t)((j0 + u) * T * 16));
-        }
-#pragma unroll
-        for (int u = 0; u < kHybStream; ++u) {
-          const int v = (j0 + u) * T + t;
-          combine_vec(wv, q[u], a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
-        }
+        for (int i = 0; i < K; ++i) qn[i] = buf_load16(rs[i], voff, (uint32_t)((j0 + 1) * T * 16));
+        const int v = j0 * T + t;
+        combine_vec(wv, q, a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
       }
     }
     __builtin_amdgcn_s_setprio(0);
