@@ -175,7 +175,7 @@ def test_golden_hand_examples():
                 np.testing.assert_allclose(a, c["alpha"], atol=1e-12)
                 np.testing.assert_allclose(a @ g, c["d"], atol=1e-12)
         elif c["name"].startswith("pcgrad"):
-            w = oracle.pcgrad(G)
+            w = oracle.pcgrad(G, np.array(c["order"]) if "order" in c else None)
             np.testing.assert_allclose(w, c["weights"], atol=1e-12)
             np.testing.assert_allclose(w @ g, c["d"], atol=1e-12)
         elif c["name"].startswith("cagrad"):
