@@ -621,6 +621,24 @@ def check_mgda_k2(fw_fn):
         assert abs(a[0] - _closed_form_k2(x[0], x[1])) <= 1e-10
 
 
+def _golden(prefix):
+    for c in json.load(open(GOLD))["cases"]:
+        if c["name"].startswith(prefix):
+            g = np.array(c["g"], dtype=np.float64)
+            yield c, g @ g.T
+
+
+def check_mgda_fw_k3(fw_fn):
+    # the hand-derived three-task Frank-Wolfe runs
+    for c, G in _golden("mgda3"):
+        np.testing.assert_allclose(fw_fn(G, 20), c["alpha"], rtol=0, atol=1e-12)
+
+
+def check_cagrad_fw_k3(ca_fn):
+    for c, G in _golden("cagrad3"):
+        np.testing.assert_allclose(ca_fn(G, c["c"], 20)[0], c["weights"], rtol=0, atol=1e-12)
+
+
 def check_pcgrad(pc_fn):
     rng = np.random.default_rng(17)
     for _ in range(10):
@@ -661,6 +679,9 @@ def test_checks_pass_on_the_oracle():
     check_pcgrad(oracle.pcgrad)
     check_cagrad(oracle.cagrad_exact)
     check_combine(oracle.combine)
+    check_mgda_fw_k3(oracle.mgda_fw)
+    check_mgda_fw_k3(_fw_copy())
+    check_cagrad_fw_k3(oracle.cagrad_fw)
     check_conflicts(oracle.conflicts)
     check_slice_offsets(oracle.slice_offsets)
     check_gram_reduce(oracle.gram_reduce)
@@ -682,6 +703,48 @@ def _fw_swapped_pair(G, iters):
         return ref.mgda_fw(G, iters)
     finally:
         ref.pair_min_norm = good
+
+
+def _fw_copy(vertex=np.argmin, line=lambda aa, ab, bb: (aa, ab, bb)):
+    """The oracle's MGDA Frank-Wolfe, restated so one step can be changed."""
+    def fw(G, iters):
+        k = G.shape[0]
+        best = None
+        for i in range(k):
+            for j in range(i + 1, k):
+                gamma, val = oracle.pair_min_norm(G[i, i], G[i, j], G[j, j])
+                if best is None or val < best[0]:
+                    best = (val, i, j, gamma)
+        _, i, j, gamma = best
+        a = np.zeros(k)
+        a[i], a[j] = gamma, 1.0 - gamma
+        for _ in range(iters):
+            ga = G @ a
+            t = int(vertex(ga))
+            gamma, _ = oracle.pair_min_norm(*line(float(a @ ga), float(ga[t]), float(G[t, t])))
+            a = gamma * a
+            a[t] += 1.0 - gamma
+        return a
+    return fw
+
+
+class _NumpyArgmax:
+    """numpy with argmin replaced by argmax."""
+    argmin = staticmethod(np.argmax)
+
+    def __getattr__(self, name):
+        return getattr(np, name)
+
+
+def _cagrad_fw_argmax(G, c, iters):
+    # mistake: the step vertex and the line-search candidate are maximisers
+    import oracle.reference as ref
+    good = ref.np
+    try:
+        ref.np = _NumpyArgmax()
+        return ref.cagrad_fw(G, c, iters)
+    finally:
+        ref.np = good
 
 
 def _pcgrad_projects_off_current(G, order):
@@ -775,6 +838,9 @@ def _gram_reduce_drops_last(parts):
 @pytest.mark.parametrize("check,mutant", [
     (check_gram, _gram_off_by_one),
     (check_mgda_k2, _fw_swapped_pair),
+    (check_mgda_fw_k3, _fw_copy(vertex=np.argmax)),
+    (check_mgda_fw_k3, _fw_copy(line=lambda aa, ab, bb: (bb, ab, aa))),
+    (check_cagrad_fw_k3, _cagrad_fw_argmax),
     (check_pcgrad, _pcgrad_projects_off_current),
     (check_pcgrad, _pcgrad_sign_flip),
     (check_cagrad, _cagrad_radius_squared),
