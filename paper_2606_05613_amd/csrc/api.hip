@@ -115,17 +115,31 @@ Carved carve(void *ws, const Layout &L) {
                 reinterpret_cast<double *>(base + L.groups), reinterpret_cast<uint32_t *>(base + L.sync)};
 }
 
+// A cooperative kernel's grid (Grid: resident_grid or hybrid_grid, K <= 4)
+// on the current device, computed once per device and instantiation; 0 if
+// the kernel cannot run there.
+template <int (*Grid)(int, int, int)>
+int cached_grid(int K, int dt, int out_dt) {
+  static std::atomic<int> cache[kMaxDevices][3][2][2];  // 0 unknown, -1 none
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    const int g = Grid(K, dt, out_dt);
+    return g > 0 ? g : 0;
+  }
+  std::atomic<int> &c = cache[dev][K - 2][dt][out_dt];
+  int g = c.load();
+  if (g == 0) {
+    g = Grid(K, dt, out_dt);
+    c.store(g > 0 ? g : -1);
+  }
+  return g > 0 ? g : 0;
+}
+
 // Workgroups for the resident path when it is forced, else 0.
 int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters) {
   (void)N, (void)B, (void)iters;
   if (g_resolve_path.load() != 2 || K > 4 || !vec || is_exact(method)) return 0;
-  static std::atomic<int> cache[3][2][2];  // K-2, dt, out_dt (device model is fixed per process here)
-  int g = cache[K - 2][dt][out_dt].load();
-  if (g == 0) {
-    g = resident_grid(K, dt, out_dt);
-    cache[K - 2][dt][out_dt].store(g > 0 ? g : -1);
-  }
-  return g > 0 ? g : 0;
+  return cached_grid<resident_grid>(K, dt, out_dt);
 }
 
 // The pipelined, partly resident path pays when each bucket carries enough
@@ -196,12 +210,7 @@ int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
                   int64_t cap_slots) {
   const int mode = g_resolve_path.load();
   if (mode == 1 || mode == 2 || K > 4 || !vec || is_exact(method)) return 0;
-  static std::atomic<int> cache[3][2][2];  // K-2, dt, out_dt
-  int g = cache[K - 2][dt][out_dt].load();
-  if (g == 0) {
-    g = hybrid_grid(K, dt, out_dt);
-    cache[K - 2][dt][out_dt].store(g > 0 ? g : -1);
-  }
+  const int g = cached_grid<hybrid_grid>(K, dt, out_dt);
   if (g <= 0) return 0;
   const int gd = hybrid_data_workgroups(g);
   if (2 * (int64_t)gd > cap_slots) return 0;
