@@ -57,3 +57,49 @@ def test_golden_resolve(case):
     want = np.array(case["d"])
     scale = max(1.0, float(np.abs(np.array(case["g"])).max()))
     assert np.all(np.abs(got - want) <= 1e-6 * scale), (case["name"], got, want)
+
+
+# Tiling a case's vectors m times multiplies every Gram entry by m.  The
+# weights of all three methods are unchanged by a common scale of G (MGDA's
+# minimiser and PCGrad's projection coefficients are scale-free; CAGrad's
+# dual objective scales by m, its radius and |g_w| each by sqrt(m)), so
+# every bucket's update is the case's d tiled.  The entries are small
+# integers and halves, exact in bf16, and every partial Gram sum stays exact
+# in fp32.  This puts the hand-derived values at full bucket sizes through
+# each resolve path.
+TILE_BUCKET = 3 << 19   # elements per bucket: whole 2- and 3-element repeats, a multiple of 8
+TILE_B = 12
+
+
+@pytest.mark.parametrize("path", ["two-pass", "resident", "hybrid"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("case", CASES, ids=[c["name"] for c in CASES])
+def test_golden_tiled(gpu_lib, case, dtype, path):
+    lib = gpu_lib
+    dev = torch.device("cuda", 0)
+    p = {"two-pass": lib.PATH_TWO_PASS, "resident": lib.PATH_RESIDENT, "hybrid": lib.PATH_HYBRID}[path]
+    m = _method(case)
+    g = torch.tensor(case["g"], dtype=torch.float64, device=dev)
+    K, dim = g.shape
+    reps = TILE_BUCKET // dim * TILE_B
+    grads = g.repeat(1, reps).to(torch.float32 if dtype == "f32" else torch.bfloat16).contiguous()
+    offs = torch.arange(TILE_B + 1, dtype=torch.int64, device=dev) * TILE_BUCKET
+    order = _order(case, dev)
+    if order is not None:
+        order = order.expand(TILE_B, K, K - 1).contiguous()
+    W = torch.empty((TILE_B, K), dtype=torch.float32, device=dev)
+    lib.set_resolve_path(p)
+    try:
+        assert lib.resolve_path(grads, TILE_B + 1, m) == p
+        out = lib.resolve(grads, offs, m, 20, case.get("c", 0.5), order, weights=W)
+        torch.cuda.synchronize()
+    finally:
+        lib.set_resolve_path(0)
+    want_w = torch.tensor(case["alpha"] if m == "mgda" else case["weights"], dtype=torch.float64, device=dev)
+    dw = (W.double() - want_w).abs() / want_w.abs().clamp(min=1.0)
+    assert float(dw.max()) <= 1e-6, (case["name"], W[0].tolist())
+    d = torch.tensor(case["d"], dtype=torch.float64, device=dev).repeat(reps)
+    scale = max(1.0, float(g.abs().max()))
+    tol = 1e-6 * scale + (2.0 ** -8 * d.abs() if dtype == "bf16" else 0.0)
+    err = (out.double() - d).abs() - tol
+    assert float(err.max()) <= 0.0, (case["name"], int(err.argmax()))
