@@ -621,21 +621,21 @@ def check_mgda_k2(fw_fn):
         assert abs(a[0] - _closed_form_k2(x[0], x[1])) <= 1e-10
 
 
-def _golden(prefix):
+def _golden(*prefixes):
     for c in json.load(open(GOLD))["cases"]:
-        if c["name"].startswith(prefix):
+        if c["name"].startswith(prefixes):
             g = np.array(c["g"], dtype=np.float64)
             yield c, g @ g.T
 
 
 def check_mgda_fw_k3(fw_fn):
-    # the hand-derived three-task Frank-Wolfe runs
-    for c, G in _golden("mgda3"):
+    # the hand-derived three- and four-task Frank-Wolfe runs
+    for c, G in _golden("mgda3", "mgda4"):
         np.testing.assert_allclose(fw_fn(G, 20), c["alpha"], rtol=0, atol=1e-12)
 
 
 def check_cagrad_fw_k3(ca_fn):
-    for c, G in _golden("cagrad3"):
+    for c, G in _golden("cagrad3", "cagrad4", "cagrad_vertex"):
         np.testing.assert_allclose(ca_fn(G, c["c"], 20)[0], c["weights"], rtol=0, atol=1e-12)
 
 
