@@ -3,8 +3,12 @@
 // d = [d_(1), ..., d_(K)]).
 //
 // Bandwidth-bound: K*N*s bytes read, N*s_out written, 2K flops per
-// element.  Same chunking and 128-bit non-temporal loads as the Gram pass;
-// the K weights of a chunk's bucket are wave-uniform scalars.
+// element.  Same chunks and 128-bit non-temporal loads as the Gram pass;
+// the K weights of a chunk's bucket are wave-uniform scalars.  Unlike the
+// Gram pass, chunks are dealt round-robin (chunk c to workgroup c mod grid),
+// so the whole grid sweeps the vector together: measured 1-2.5% faster
+// than one contiguous run per workgroup on every workload shape here, in
+// fast and slow buffer placements alike (the Gram pass gains nothing).
 //
 // Arithmetic.  For an fp32 output the sum is an fp32 FMA chain in task
 // order.  For a bf16 output that is not enough: with bf16 inputs the exact
@@ -31,14 +35,11 @@ __global__ __launch_bounds__(kThreads) void combine_kernel(
   constexpr int64_t C = combine_chunk_elems(K, DT);
   constexpr int EB = elem_bytes(DT);
 
-  int64_t c, cend;
-  my_chunks(cs[B], c, cend);
-  if (c >= cend) return;
-  int b = find_bucket(cs, B, c);
+  const int64_t total = cs[B];
   const int tid = threadIdx.x;
 
-  for (; c < cend; ++c) {
-    while (cs[b + 1] <= c) ++b;
+  for (int64_t c = blockIdx.x; c < total; c += gridDim.x) {
+    const int b = find_bucket(cs, B, c);
     const int64_t lo = offs[b] + (c - cs[b]) * C;
     const int64_t hi = lo + C < offs[b + 1] ? lo + C : offs[b + 1];
     float w[K];
