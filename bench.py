@@ -322,8 +322,9 @@ def main():
         e1.record(stream)
         torch.cuda.synchronize()
         extras[name] = round(e0.elapsed_time(e1) / 3, 4)
+    per_bucket = f", per-bucket Gram {st['gram']:.3f} ms" if "gram" in st else ""
     log(f"sliced Gram (T=8) {extras['gram_sliced_T8']:.3f} ms, global Gram (B=1) "
-        f"{extras['gram_global_B1']:.3f} ms, per-bucket Gram {st.get('gram', float('nan')):.3f} ms")
+        f"{extras['gram_global_B1']:.3f} ms{per_bucket}")
     del ws8, P8, ws1
 
     # dominant kernel: the cooperative kernel (credited with the one-read

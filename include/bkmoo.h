@@ -30,6 +30,11 @@
  *     allocates every buffer; the library never allocates, frees or
  *     synchronises inside these calls, and all work is queued on `stream`
  *     (asynchronous; results are valid once the stream reaches that point).
+ *   - Device pointers must be memory of the current HIP device (hipGetDevice)
+ *     and `stream` must belong to it: launch grids are sized from that
+ *     device's compute units and occupancy.  The library cannot tell a host
+ *     or foreign pointer from a device one; passing one is undefined (a GPU
+ *     memory fault).
  *   - grads is a HOST array of K device pointers, one per task, each to N
  *     elements of dtype `dt`.  A contiguous [K][N] buffer is passed as
  *     base + i*N*elem_size.  Rows need natural alignment (4 bytes for f32,

@@ -133,6 +133,21 @@ def _rows(grads: Grads):
     return arr, dt, len(rows), n, dev, rows
 
 
+def _gpu(t: torch.Tensor, what: str):
+    """The GPU device of t; host tensors are refused (the kernels would
+    dereference their pointers on the GPU)."""
+    if t.device.type != "cuda":
+        raise ValueError(f"{what} must be on a GPU")
+    return t.device
+
+
+def _tensor(t: torch.Tensor, shape, dtype, dev, what: str) -> int:
+    """Pointer of a caller-supplied tensor that must match exactly."""
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or t.device != dev:
+        raise ValueError(f"{what} must be a contiguous {dtype} tensor of shape {tuple(shape)} on {dev}")
+    return t.data_ptr()
+
+
 def _offsets(offsets: torch.Tensor, dev) -> torch.Tensor:
     if offsets.dtype != torch.int64 or offsets.dim() != 1 or offsets.device != dev \
             or not offsets.is_contiguous():
@@ -140,13 +155,10 @@ def _offsets(offsets: torch.Tensor, dev) -> torch.Tensor:
     return offsets
 
 
-def _hparams(max_iter: int, cagrad_c: float, pcgrad_order: Optional[torch.Tensor], K: int, B: int):
+def _hparams(max_iter: int, cagrad_c: float, pcgrad_order: Optional[torch.Tensor], K: int, B: int, dev):
     ptr = None
     if pcgrad_order is not None:
-        if pcgrad_order.dtype != torch.int8 or tuple(pcgrad_order.shape) != (B, K, K - 1) \
-                or not pcgrad_order.is_contiguous() or pcgrad_order.device.type != "cuda":
-            raise ValueError("pcgrad_order must be a contiguous int8 [B, K, K-1] GPU tensor")
-        ptr = pcgrad_order.data_ptr()
+        ptr = _tensor(pcgrad_order, (B, K, K - 1), torch.int8, dev, "pcgrad_order")
     return _Hparams(int(max_iter), float(cagrad_c), ptr)
 
 
@@ -174,9 +186,11 @@ def gram(grads: Grads, bucket_offsets: torch.Tensor, gram_out: Optional[torch.Te
     B = offs.numel() - 1
     if gram_out is None:
         gram_out = torch.empty((B, K, K), dtype=torch.float64, device=dev)
+    _tensor(gram_out, (B, K, K), torch.float64, dev, "gram_out")
     ws = _workspace(workspace, K, N, B, dt, dev)
-    _check(_lib.bkmoo_gram(K, arr, dt, N, B, offs.data_ptr(), gram_out.data_ptr(), ws.data_ptr(),
-                           ws.numel(), _stream_ptr(dev)), "bkmoo_gram")
+    with torch.cuda.device(dev):
+        _check(_lib.bkmoo_gram(K, arr, dt, N, B, offs.data_ptr(), gram_out.data_ptr(), ws.data_ptr(),
+                               ws.numel(), _stream_ptr(dev)), "bkmoo_gram")
     return gram_out
 
 
@@ -187,14 +201,17 @@ def solve(gram_in: torch.Tensor, method: str, max_iter: int = 20, cagrad_c: floa
     if gram_in.dtype != torch.float64 or gram_in.dim() != 3 or not gram_in.is_contiguous():
         raise ValueError("gram must be a contiguous fp64 [B, K, K] tensor")
     B, K, _ = gram_in.shape
-    dev = gram_in.device
+    dev = _gpu(gram_in, "gram")
     if weights is None:
         weights = torch.empty((B, K), dtype=torch.float32, device=dev)
     if aux is None:
         aux = torch.empty((B, K), dtype=torch.float64, device=dev)
-    hp = _hparams(max_iter, cagrad_c, pcgrad_order, K, B)
-    _check(_lib.bkmoo_solve(K, B, gram_in.data_ptr(), METHODS[method], ctypes.byref(hp),
-                            weights.data_ptr(), aux.data_ptr(), _stream_ptr(dev)), "bkmoo_solve")
+    _tensor(weights, (B, K), torch.float32, dev, "weights")
+    _tensor(aux, (B, K), torch.float64, dev, "aux")
+    hp = _hparams(max_iter, cagrad_c, pcgrad_order, K, B, dev)
+    with torch.cuda.device(dev):
+        _check(_lib.bkmoo_solve(K, B, gram_in.data_ptr(), METHODS[method], ctypes.byref(hp),
+                                weights.data_ptr(), aux.data_ptr(), _stream_ptr(dev)), "bkmoo_solve")
     return weights, aux
 
 
@@ -209,8 +226,9 @@ def slice_offsets(bucket_offsets: torch.Tensor, T: int) -> torch.Tensor:
         raise ValueError("bucket_offsets must be a contiguous int64 GPU tensor")
     B = offs.numel() - 1
     out = torch.empty(B * T + 1, dtype=torch.int64, device=offs.device)
-    _check(_lib.bkmoo_slice_offsets(B, int(T), offs.data_ptr(), out.data_ptr(), _stream_ptr(offs.device)),
-           "bkmoo_slice_offsets")
+    with torch.cuda.device(offs.device):
+        _check(_lib.bkmoo_slice_offsets(B, int(T), offs.data_ptr(), out.data_ptr(), _stream_ptr(offs.device)),
+               "bkmoo_slice_offsets")
     return out
 
 
@@ -224,10 +242,13 @@ def gram_reduce(partial: torch.Tensor, layout: int = SLICES_RANK_MAJOR,
         T, B, K, _ = partial.shape
     else:
         B, T, K, _ = partial.shape
+    dev = _gpu(partial, "partial")
     if gram_out is None:
-        gram_out = torch.empty((B, K, K), dtype=torch.float64, device=partial.device)
-    _check(_lib.bkmoo_gram_reduce(K, B, T, partial.data_ptr(), int(layout), gram_out.data_ptr(),
-                                  _stream_ptr(partial.device)), "bkmoo_gram_reduce")
+        gram_out = torch.empty((B, K, K), dtype=torch.float64, device=dev)
+    _tensor(gram_out, (B, K, K), torch.float64, dev, "gram_out")
+    with torch.cuda.device(dev):
+        _check(_lib.bkmoo_gram_reduce(K, B, T, partial.data_ptr(), int(layout), gram_out.data_ptr(),
+                                      _stream_ptr(dev)), "bkmoo_gram_reduce")
     return gram_out
 
 
@@ -240,13 +261,14 @@ def conflicts(gram_in: torch.Tensor, cosines: bool = True, summary: bool = True,
     if gram_in.dtype != torch.float64 or gram_in.dim() != 3 or not gram_in.is_contiguous():
         raise ValueError("gram must be a contiguous fp64 [B, K, K] tensor")
     B, K, _ = gram_in.shape
-    dev = gram_in.device
+    dev = _gpu(gram_in, "gram")
     cos = torch.empty((B, K, K), dtype=torch.float64, device=dev) if cosines else None
     summ = torch.empty((B, 3), dtype=torch.float64, device=dev) if summary else None
     prs = torch.empty((B, 3), dtype=torch.int32, device=dev) if pairs else None
     ptr = lambda t: t.data_ptr() if t is not None else None
-    _check(_lib.bkmoo_conflicts(K, B, gram_in.data_ptr(), ptr(cos), ptr(summ), ptr(prs),
-                                _stream_ptr(dev)), "bkmoo_conflicts")
+    with torch.cuda.device(dev):
+        _check(_lib.bkmoo_conflicts(K, B, gram_in.data_ptr(), ptr(cos), ptr(summ), ptr(prs),
+                                    _stream_ptr(dev)), "bkmoo_conflicts")
     return cos, summ, prs
 
 
@@ -257,14 +279,15 @@ def combine(grads: Grads, bucket_offsets: torch.Tensor, weights: torch.Tensor,
     arr, dt, K, N, dev, _ = _rows(grads)
     offs = _offsets(bucket_offsets, dev)
     B = offs.numel() - 1
-    if weights.dtype != torch.float32 or tuple(weights.shape) != (B, K) or not weights.is_contiguous():
-        raise ValueError("weights must be a contiguous fp32 [B, K] tensor")
+    _tensor(weights, (B, K), torch.float32, dev, "weights")
     if out is None:
         out = torch.empty(N, dtype=out_dtype or _torch_dt(dt), device=dev)
     odt = _dt(out)
+    _tensor(out, (N,), out.dtype, dev, "out")
     ws = _workspace(workspace, K, N, B, dt, dev)
-    _check(_lib.bkmoo_combine(K, arr, dt, N, B, offs.data_ptr(), weights.data_ptr(), out.data_ptr(),
-                              odt, ws.data_ptr(), ws.numel(), _stream_ptr(dev)), "bkmoo_combine")
+    with torch.cuda.device(dev):
+        _check(_lib.bkmoo_combine(K, arr, dt, N, B, offs.data_ptr(), weights.data_ptr(), out.data_ptr(),
+                                  odt, ws.data_ptr(), ws.numel(), _stream_ptr(dev)), "bkmoo_combine")
     return out
 
 
@@ -281,27 +304,28 @@ def resolve(grads: Grads, bucket_offsets: torch.Tensor, method: str, max_iter: i
     if out is None:
         out = torch.empty(N, dtype=out_dtype or _torch_dt(dt), device=dev)
     odt = _dt(out)
+    _tensor(out, (N,), out.dtype, dev, "out")
     ws = _workspace(workspace, K, N, B, dt, dev)
-    hp = _hparams(max_iter, cagrad_c, pcgrad_order, K, B)
+    hp = _hparams(max_iter, cagrad_c, pcgrad_order, K, B, dev)
 
-    def ptr(t, shape, dtype):
-        if t is None:
-            return None
-        if t.dtype != dtype or tuple(t.shape) != shape or not t.is_contiguous() or t.device != dev:
-            raise ValueError(f"expected a contiguous {dtype} {shape} tensor")
-        return t.data_ptr()
+    def ptr(t, shape, dtype, what):
+        return None if t is None else _tensor(t, shape, dtype, dev, what)
 
-    _check(_lib.bkmoo_resolve(K, arr, dt, N, B, offs.data_ptr(), METHODS[method], ctypes.byref(hp),
-                              out.data_ptr(), odt, ptr(gram_out, (B, K, K), torch.float64),
-                              ptr(weights, (B, K), torch.float32), ptr(aux, (B, K), torch.float64),
-                              ws.data_ptr(), ws.numel(), _stream_ptr(dev)), "bkmoo_resolve")
+    with torch.cuda.device(dev):
+        _check(_lib.bkmoo_resolve(K, arr, dt, N, B, offs.data_ptr(), METHODS[method], ctypes.byref(hp),
+                                  out.data_ptr(), odt, ptr(gram_out, (B, K, K), torch.float64, "gram_out"),
+                                  ptr(weights, (B, K), torch.float32, "weights"),
+                                  ptr(aux, (B, K), torch.float64, "aux"),
+                                  ws.data_ptr(), ws.numel(), _stream_ptr(dev)), "bkmoo_resolve")
     return out
 
 
 def read_device_error(workspace: torch.Tensor) -> int:
     v = ctypes.c_uint32(0)
-    _check(_lib.bkmoo_read_device_error(workspace.data_ptr(), ctypes.byref(v),
-                                        _stream_ptr(workspace.device)), "bkmoo_read_device_error")
+    dev = _gpu(workspace, "workspace")
+    with torch.cuda.device(dev):
+        _check(_lib.bkmoo_read_device_error(workspace.data_ptr(), ctypes.byref(v), _stream_ptr(dev)),
+               "bkmoo_read_device_error")
     return v.value
 
 

@@ -199,3 +199,14 @@ def test_binding_rejects_bad_tensors_on_cpu(b):
         b.gram(torch.zeros((2, 8)), torch.zeros(2, dtype=torch.int64))   # CPU rows
     with pytest.raises(TypeError):
         b.gram(torch.zeros((2, 8), dtype=torch.float16), torch.zeros(2, dtype=torch.int64))
+    # host tensors are refused before any call reaches the library
+    G = torch.zeros((3, 2, 2), dtype=torch.float64)
+    for call in (lambda: b.solve(G, "mgda"), lambda: b.conflicts(G),
+                 lambda: b.gram_reduce(torch.zeros((2, 3, 2, 2), dtype=torch.float64)),
+                 lambda: b.read_device_error(torch.zeros(256, dtype=torch.uint8)),
+                 lambda: b.slice_offsets(torch.zeros(4, dtype=torch.int64), 2),
+                 lambda: b.combine(torch.zeros((2, 8)), torch.zeros(2, dtype=torch.int64),
+                                   torch.zeros((1, 2))),
+                 lambda: b.resolve(torch.zeros((2, 8)), torch.zeros(2, dtype=torch.int64), "mgda")):
+        with pytest.raises(ValueError, match="GPU"):
+            call()
