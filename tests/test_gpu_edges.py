@@ -1,6 +1,7 @@
 """GPU edge cases: invalid offsets, non-finite inputs, misaligned and
 separately allocated rows, in-place update, one global bucket, empty input,
-degenerate Gram matrices and invalid PCGrad orders."""
+degenerate Gram matrices, invalid PCGrad orders and mismatched output
+tensors refused by the binding."""
 
 import numpy as np
 import pytest
@@ -155,3 +156,30 @@ def test_invalid_pcgrad_order_gives_nan_weights(gpu_lib):
     W, _ = gpu_lib.solve(G, "pcgrad", pcgrad_order=order)
     torch.cuda.synchronize()
     assert torch.all(W[0] == 1) and torch.isnan(W[1]).all() and torch.isnan(W[2]).all()
+
+
+def test_binding_refuses_mismatched_outputs(gpu_lib):
+    """Outputs and parameters on the host, or of the wrong shape or type,
+    are refused before any call reaches the library; the inputs stay intact."""
+    K, N, B = 3, 4096, 2
+    g = torch.randn((K, N), device="cuda")
+    keep = g.clone()
+    offs = torch.tensor([0, 1000, N], dtype=torch.int64, device="cuda")
+    bad_calls = [
+        lambda: gpu_lib.resolve(g, offs, "mgda", out=torch.empty(N)),
+        lambda: gpu_lib.resolve(g, offs, "mgda", out=torch.empty(N - 1, device="cuda")),
+        lambda: gpu_lib.resolve(g, offs, "mgda", weights=torch.empty((B, K))),
+        lambda: gpu_lib.resolve(g, offs, "mgda", gram_out=torch.empty((B, K, K), device="cuda")),
+        lambda: gpu_lib.resolve(g, offs, "pcgrad", pcgrad_order=torch.zeros((B, K, K - 1), dtype=torch.int8)),
+        lambda: gpu_lib.gram(g, offs, gram_out=torch.empty((B + 1, K, K), dtype=torch.float64, device="cuda")),
+        lambda: gpu_lib.combine(g, offs, torch.full((B, K), 0.5)),
+        lambda: gpu_lib.combine(g, offs, torch.full((B, K), 0.5, device="cuda"),
+                                out=torch.empty((1, N), device="cuda")),
+        lambda: gpu_lib.solve(torch.eye(K, dtype=torch.float64, device="cuda").expand(B, K, K).contiguous(),
+                              "mgda", weights=torch.empty((B, K), dtype=torch.float64, device="cuda")),
+    ]
+    for call in bad_calls:
+        with pytest.raises(ValueError):
+            call()
+    torch.cuda.synchronize()
+    assert torch.equal(g, keep)
