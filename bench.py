@@ -138,9 +138,9 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): this build has no multi-GPU "
-              "path; the bucket-level resolve shards by buckets and bucket slices, which is described "
-              "but not built.", flush=True)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the library has no multi-GPU "
+              "path (the bucket-level resolve would shard by buckets and bucket slices; not "
+              "implemented).", flush=True)
         sys.exit(2)
 
     import torch
