@@ -21,9 +21,11 @@ Reported next to the throughput:
                it must move (Gram K*s*N, combine (K+1)*s*N); a cooperative
                kernel, which does the whole step, counts the one-read floor
                K*s*N + s_out*N and gets no credit for its re-reads, part of
-               which the last-level cache serves.  `traffic` (HBM bytes per
-               launch) comes from the committed rocprofv3 counter summary
-               when it matches the current kernel source, else null;
+               which the last-level cache serves (`requested_frac`: the
+               bytes it does request, re-reads included, per launch
+               duration, over 8 TB/s).  `traffic` (HBM bytes per launch)
+               comes from the committed rocprofv3 counter summary when it
+               matches the current kernel source, else null;
   two_pass     when the step ran a cooperative kernel: the plain two-pass
                resolve on the same inputs, with its (2K+1)*s*N bytes;
   cpu_baseline the float64 oracle on a bounded prefix of the same buckets,
@@ -341,6 +343,12 @@ def main():
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
             "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic, "kernel": kname,
             "algorithmic_bytes_per_launch": kbytes, "avg_launch_ms": round(kms, 4)}
+    if cooperative:
+        # what the kernel draws from memory (one read, the second read of the
+        # part it did not keep on chip, the update) over peak, beside the
+        # one-read credit above
+        roof["requested_bytes_per_launch"] = traffic_bytes
+        roof["requested_frac"] = round(traffic_bytes / (kms / 1e3) / 1e9 / PEAK_HBM_GBPS, 4)
     result = {
         "metric": METRIC,
         "value": K * N / (ms_step / 1e3),
