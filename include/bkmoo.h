@@ -89,7 +89,7 @@ typedef enum {
 
 /* Device error word bits (bkmoo_read_device_error). */
 #define BKMOO_DEVERR_OFFSETS 0x1u /* bucket offsets rejected */
-#define BKMOO_DEVERR_TIMEOUT 0x2u /* single-read resolve: a bounded wait expired (results invalid) */
+#define BKMOO_DEVERR_TIMEOUT 0x2u /* a cooperative resolve's bounded wait expired (results invalid) */
 
 /* Layout of T sets of per-slice partial Gram matrices (bkmoo_gram_reduce). */
 typedef enum {
