@@ -217,24 +217,24 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  * Three implementations, same definitions and tolerances:
  *   two-pass  the kernels of bkmoo_gram, bkmoo_solve and bkmoo_combine;
  *             results equal those three calls bitwise.
- *   hybrid    (K <= 4, 16-byte-phase-aligned rows and output) one
+ *   hybrid    (K <= 8, 16-byte-phase-aligned rows and output) one
  *             cooperative kernel in which the Gram pass of bucket b+1 runs
- *             while bucket b is solved; about half of each bucket stays on
- *             chip between its Gram and its combine and the rest is read
- *             again (mostly from the last-level cache).  The Gram sums run
- *             in a different (also fixed) order, so results agree with the
- *             two-pass path to rounding, not bitwise; they depend on the
- *             device's CU count and, for K = 4 with MGDA or CAGrad, on the
- *             segment layout the method selects (deterministic for given
- *             arguments).
+ *             while bucket b is solved; part of each bucket (about half at
+ *             K <= 4, less for more tasks) stays on chip between its Gram
+ *             and its combine and the rest is read again (partly from the
+ *             last-level cache).  The Gram sums run in a different (also
+ *             fixed) order, so results agree with the two-pass path to
+ *             rounding, not bitwise; they depend on the device's CU count
+ *             and, for K >= 4 with MGDA or CAGrad, on the segment layout
+ *             the method selects (deterministic for given arguments).
  *   resident  (K <= 4, aligned as above) one cooperative kernel keeps each
  *             bucket in registers and LDS between its Gram and its combine,
  *             so every gradient element is read from HBM once (a bucket
  *             larger than the chip holds is read twice, still correct);
  *             same agreement with the two-pass path.
  * Automatic choice: the hybrid path for at least 8 buckets of which at
- * least 10% stays on chip, averaging (all K rows) at least 24 MiB plus
- * 4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA
+ * least 10% stays on chip, averaging (all K rows) at least max(24, 6 K)
+ * MiB plus 4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA
  * iteration, 0.22 K us per CAGrad iteration, 0.1 K^2 us for PCGrad, 0 for
  * the mean), so that each bucket's hand-off is amortised; else the two
  * passes.  Exact solvers never take a cooperative path.  The resident
@@ -333,7 +333,8 @@ bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *c
  * workgroup of each CU takes a longer segment.  BKMOO_EINVAL
  * for bad sizes or pointers, invalid offsets, method or iteration count, or
  * an unknown path;
- * BKMOO_EUNSUPPORTED for a cooperative path with K > 4; BKMOO_EHIP when the
+ * BKMOO_EUNSUPPORTED for the resident path with K > 4 or the hybrid path
+ * with K > 8; BKMOO_EHIP when the
  * current device cannot be queried.
  */
 bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_t *offsets_host,
@@ -369,7 +370,7 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
 /*
  * bkmoo_set_resolve_path — force bkmoo_resolve's implementation
  * (0: automatic, BKMOO_PATH_TWO_PASS, BKMOO_PATH_RESIDENT or
- * BKMOO_PATH_HYBRID when eligible: K <= 4, aligned rows, not an exact
+ * BKMOO_PATH_HYBRID when eligible: K <= 8 (resident K <= 4), aligned rows, not an exact
  * method; the resident path is taken only when forced).  Process-wide; for
  * tests and tuning.
  */

@@ -115,12 +115,12 @@ Carved carve(void *ws, const Layout &L) {
                 reinterpret_cast<double *>(base + L.groups), reinterpret_cast<uint32_t *>(base + L.sync)};
 }
 
-// A cooperative kernel's grid (Grid: resident_grid or hybrid_grid, K <= 4)
+// A cooperative kernel's grid (Grid: resident_grid or hybrid_grid)
 // on the current device, computed once per device and instantiation; 0 if
 // the kernel cannot run there.
 template <int (*Grid)(int, int, int)>
 int cached_grid(int K, int dt, int out_dt) {
-  static std::atomic<int> cache[kMaxDevices][3][2][2];  // 0 unknown, -1 none
+  static std::atomic<int> cache[kMaxDevices][kHybridMaxK - 1][2][2];  // K-2, dt, out_dt: 0 unknown, -1 none
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
     const int g = Grid(K, dt, out_dt);
@@ -162,6 +162,7 @@ int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int m
 // on chip and lose.
 constexpr int kHybridMinBuckets = 8;
 constexpr double kHybridBaseMiB = 24.0;   // all K rows, no solve
+constexpr double kHybridBaseMiBPerRow = 6.0;  // ... and at least this per row (K > 4)
 constexpr double kHybridMiBPerUs = 4.0;   // per microsecond of solve latency
 constexpr double kHybridMinHeld = 0.1;    // fraction of a bucket kept on chip
 
@@ -173,11 +174,13 @@ constexpr double kHybridMinHeld = 0.1;    // fraction of a bucket kept on chip
 // and 16 MiB buckets 7% lower, but slows the mean method by 2-5%, 50 MiB
 // CAGrad by 5%, 100 MiB buckets by 2%, and K = 2 or 3 by 5-30% (their
 // second workgroups' segments would no longer fill what they keep on chip).
+// At K = 8 it takes 25 MiB CAGrad FW-20 buckets from 40.8 to 39.2 ms; it
+// applies from K = 4 up.
 constexpr int kHybridSkewPm = 350;
 constexpr double kHybridSkewMaxRowBytes = 32.0 * (1 << 20);
 
 int hybrid_skew_pm(int K, int dt, int method, int iters, int64_t N, int B, int grid) {
-  if (K != 4 || (method != BKMOO_MGDA && method != BKMOO_CAGRAD) || iters <= 0 || B <= 0) return 0;
+  if (K < 4 || (method != BKMOO_MGDA && method != BKMOO_CAGRAD) || iters <= 0 || B <= 0) return 0;
   const double avg = (double)N / B;
   if (avg * elem_bytes(dt) > kHybridSkewMaxRowBytes) return 0;
   const int gd = hybrid_data_workgroups(grid), older = hybrid_older_workgroups(grid);
@@ -209,7 +212,7 @@ double solve_latency_us(int method, int K, int iters) {
 int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters,
                   int64_t cap_slots) {
   const int mode = g_resolve_path.load();
-  if (mode == 1 || mode == 2 || K > 4 || !vec || is_exact(method)) return 0;
+  if (mode == 1 || mode == 2 || K > kHybridMaxK || !vec || is_exact(method)) return 0;
   const int g = cached_grid<hybrid_grid>(K, dt, out_dt);
   if (g <= 0) return 0;
   const int gd = hybrid_data_workgroups(g);
@@ -219,7 +222,8 @@ int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
   const double avg_elems = (double)N / B;
   const double bucket_bytes = avg_elems * K * elem_bytes(dt);
   const double held = (double)hybrid_held_elems(K, dt) * gd / (avg_elems > 1.0 ? avg_elems : 1.0);
-  const double min_bytes = (kHybridBaseMiB + kHybridMiBPerUs * solve_latency_us(method, K, iters)) * (1 << 20);
+  const double base_mib = kHybridBaseMiB > kHybridBaseMiBPerRow * K ? kHybridBaseMiB : kHybridBaseMiBPerRow * K;
+  const double min_bytes = (base_mib + kHybridMiBPerUs * solve_latency_us(method, K, iters)) * (1 << 20);
   return B >= kHybridMinBuckets && bucket_bytes >= min_bytes && held >= kHybridMinHeld ? g : 0;
 }
 
@@ -418,7 +422,7 @@ bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_
     return BKMOO_OK;
   }
   if (path != BKMOO_PATH_RESIDENT && path != BKMOO_PATH_HYBRID) return BKMOO_EINVAL;
-  if (K > 4) return BKMOO_EUNSUPPORTED;
+  if (K > (path == BKMOO_PATH_RESIDENT ? 4 : kHybridMaxK)) return BKMOO_EUNSUPPORTED;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return BKMOO_EHIP;
   uint64_t reread = 0;  // elements read a second time

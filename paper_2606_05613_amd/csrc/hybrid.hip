@@ -10,8 +10,8 @@
 // buckets: the data of bucket b+1 streams in while bucket b's weights are
 // produced, and bucket b's combine re-reads only the part it did not keep.
 //
-// How.  Workgroups of 256 threads, two per CU (two can sit in different
-// phases, so one computes while the other streams).  The first kHybSolvers
+// How.  K <= 8.  Workgroups of 256 threads, two per CU (two can sit in
+// different phases, so one computes while the other streams).  The first kHybSolvers
 // workgroups of the grid hold no data: solver j
 // takes buckets j, j + kHybSolvers, ...; it waits until every data workgroup
 // has stored its partial Gram of the bucket, adds the partials in a fixed
@@ -57,16 +57,21 @@ namespace {
 constexpr int kHybThreads = 256;  // two workgroups per CU
 constexpr int kHybWaves = kHybThreads / kWave;
 constexpr int kHybSolvers = 4;  // workgroups that reduce and solve, holding no data
-constexpr int kHybStream = 2;   // streamed vectors per task row and thread per Gram-phase step
 // Partials a solver thread loads at once: with one segment per data
 // workgroup (~508) and 25 threads per Gram entry, one round trip.
 constexpr int kHybRedBatch = 24;
 
 // Vectors per task row and thread kept in each of the two buffers: registers
-// (NR) and LDS (NL).  The two buffers together hold about what the
-// single-read kernel holds for one bucket.
-constexpr int hyb_regs(int K) { return K <= 2 ? 9 : K == 3 ? 6 : 4; }
-constexpr int hyb_lds(int K) { return K <= 2 ? 4 : 2; }
+// (NR) and LDS (NL), and streamed per row and Gram-phase step (NS).  At
+// K <= 4 the two buffers together hold about what the single-read kernel
+// holds for one bucket.  Above that registers run short, and keeping loads
+// in flight comes first: a wavefront streams NS * K vectors at a time, and
+// with fewer than ~10 in flight the kernel falls behind the two passes
+// (K = 5 and 6 with NS = 1: 5-25% slower; with NS = 2 and NR = 2: 8-30%
+// faster).  K = 8 fits only NR = NL = NS = 1 (its 8 loads in flight).
+constexpr int hyb_regs(int K) { return K <= 2 ? 9 : K == 3 ? 6 : K == 4 ? 4 : K <= 6 ? 2 : 1; }
+constexpr int hyb_lds(int K) { return K <= 2 ? 4 : K <= 4 ? 2 : 1; }
+constexpr int hyb_stream(int K) { return K <= 7 ? 2 : 1; }
 
 struct HybArgs {
   const int64_t *offs;  // [B+1]
@@ -114,6 +119,7 @@ struct Hybrid {
   static constexpr int NR = hyb_regs(K);
   static constexpr int NL = hyb_lds(K);
   static constexpr int NB = NR + NL;
+  static constexpr int NS = hyb_stream(K);
   static constexpr int P = pairs(K);
   static constexpr int T = kHybThreads;
   static constexpr int EB = elem_bytes(DT);
@@ -171,19 +177,19 @@ struct Hybrid {
           for (int i = 0; i < K; ++i) sm.lds[X][j][i][t] = stage[j][i];
         }
       }
-      // streamed vectors, kHybStream per row at a time; loaded with the
+      // streamed vectors, NS per row at a time; loaded with the
       // temporal policy so that the combine's re-read, one bucket later, is
       // mostly served by the last-level cache instead of HBM
       const int nslot = (sp.nv + T - 1) / T;
-      for (int j0 = NB; j0 < nslot; j0 += kHybStream) {
-        u32x4 q[kHybStream][K];
+      for (int j0 = NB; j0 < nslot; j0 += NS) {
+        u32x4 q[NS][K];
 #pragma unroll
-        for (int u = 0; u < kHybStream; ++u) {
+        for (int u = 0; u < NS; ++u) {
 #pragma unroll
           for (int i = 0; i < K; ++i) q[u][i] = buf_load16_keep(rs[i], voff, (uint32_t)((j0 + u) * T * 16));
         }
 #pragma unroll
-        for (int u = 0; u < kHybStream; ++u) accumulate_vec(acc, q[u]);
+        for (int u = 0; u < NS; ++u) accumulate_vec(acc, q[u]);
       }
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
@@ -452,7 +458,9 @@ int hybrid_grid_t() {
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, hybrid_kernel<K, DT, ODT>, kHybThreads, 0) !=
       hipSuccess)
     return 0;
-  const int g = occ * device_cu_count();
+  // two workgroups per CU, the layout the kernel is built for (a lighter
+  // instantiation could fit three, which only adds contention)
+  const int g = (occ < 2 ? occ : 2) * device_cu_count();
   return g > 2 * kHybSolvers ? g : 0;
 }
 
@@ -467,6 +475,10 @@ int hybrid_grid(int K, int dt, int out_dt) {
     BKMOO_HYB_CASE(2)
     BKMOO_HYB_CASE(3)
     BKMOO_HYB_CASE(4)
+    BKMOO_HYB_CASE(5)
+    BKMOO_HYB_CASE(6)
+    BKMOO_HYB_CASE(7)
+    BKMOO_HYB_CASE(8)
     default: return 0;
   }
 #undef BKMOO_HYB_CASE
@@ -507,6 +519,10 @@ hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, con
     BKMOO_HYB_CASE(2)
     BKMOO_HYB_CASE(3)
     BKMOO_HYB_CASE(4)
+    BKMOO_HYB_CASE(5)
+    BKMOO_HYB_CASE(6)
+    BKMOO_HYB_CASE(7)
+    BKMOO_HYB_CASE(8)
     default: return hipErrorInvalidValue;
   }
 #undef BKMOO_HYB_CASE

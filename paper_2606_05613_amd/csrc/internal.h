@@ -10,6 +10,7 @@ namespace bkmoo {
 constexpr int kMinK = 2;
 constexpr int kMaxK = 16;
 constexpr int kExactMaxK = 10;  // exact solvers: 2^K - 1 supports per bucket
+constexpr int kHybridMaxK = 8;  // the pipelined cooperative resolve (hybrid.hip)
 constexpr int kThreads = 256;          // streaming kernels: 4 wavefronts of 64
 constexpr int kWave = 64;
 

@@ -1,7 +1,7 @@
 """The automatic choice between the resolve paths (bkmoo_resolve_path) on
-MI355X shapes: the hybrid path needs at least 8 buckets, at least 10% of a
-bucket kept on chip, and buckets (all K rows) of at least 24 MiB plus
-4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA and
+MI355X shapes: the hybrid path (K <= 8) needs at least 8 buckets, at least
+10% of a bucket kept on chip, and buckets (all K rows) of at least
+max(24, 6 K) MiB plus 4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA and
 0.22 K us per CAGrad iteration, 0.1 K^2 us for PCGrad); everything else
 runs the two passes.  The single-read resident kernel runs only when
 forced.  Only shapes are used (no resolve runs); the cases sit away from
@@ -49,6 +49,46 @@ def test_automatic_path(gpu_lib, rows_4x2g, B, method, iters, want):
     gpu_lib.set_resolve_path(0)
     got = names[gpu_lib.resolve_path(rows_4x2g, B + 1, method, iters)]
     assert got == want, f"B={B} {method}-{iters}: {got}"
+
+
+# (K, buckets, method, iterations, expected path name); rows of 2^28 bf16
+# elements (512 MiB).  Each case's side was measured on MI355X: at K = 8
+# the pipelined kernel loses at 4 MiB per row, wins at 8-25 MiB when the
+# solve is short enough, and keeps too little on chip at 50 MiB.
+CASES_MORE_TASKS = [
+    (8, 128, "mean", 0, "two-pass"),   # 32 MiB buckets < 48 (6 MiB per row)
+    (8, 64, "mean", 0, "hybrid"),      # 64 MiB >= 48
+    (8, 64, "mgda", 20, "two-pass"),   # 64 < 48 + 4 * 11.2
+    (8, 32, "mgda", 20, "hybrid"),     # 128 >= 92.8
+    (8, 32, "pcgrad", 0, "hybrid"),    # 128 >= 48 + 4 * 6.4
+    (8, 32, "cagrad", 20, "two-pass"), # 128 < 48 + 4 * 35.2
+    (8, 20, "cagrad", 20, "hybrid"),   # 204.8 >= 188.8
+    (8, 10, "mean", 0, "two-pass"),    # 51 MiB per row: < 10% kept on chip
+    (6, 64, "mean", 0, "hybrid"),      # 48 MiB >= 36
+    (6, 128, "mean", 0, "two-pass"),   # 24 MiB < 36
+    (5, 32, "mgda", 20, "hybrid"),     # 80 MiB >= 30 + 4 * 7
+]
+
+
+@pytest.mark.parametrize("K,B,method,iters,want", CASES_MORE_TASKS)
+def test_automatic_path_more_tasks(gpu_lib, K, B, method, iters, want):
+    names = {gpu_lib.PATH_TWO_PASS: "two-pass", gpu_lib.PATH_RESIDENT: "resident",
+             gpu_lib.PATH_HYBRID: "hybrid"}
+    g = torch.empty((K, 1 << 28), dtype=torch.bfloat16, device="cuda")
+    gpu_lib.set_resolve_path(0)
+    got = names[gpu_lib.resolve_path(g, B + 1, method, iters)]
+    assert got == want, f"K={K} B={B} {method}-{iters}: {got}"
+
+
+def test_more_than_eight_tasks_run_two_passes(gpu_lib):
+    g = torch.empty((9, 1 << 26), dtype=torch.bfloat16, device="cuda")
+    gpu_lib.set_resolve_path(0)
+    assert gpu_lib.resolve_path(g, 9, "mean", 0) == gpu_lib.PATH_TWO_PASS
+    gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
+    try:
+        assert gpu_lib.resolve_path(g, 9, "mean", 0) == gpu_lib.PATH_TWO_PASS
+    finally:
+        gpu_lib.set_resolve_path(0)
 
 
 def test_hybrid_needs_a_tenth_on_chip(gpu_lib):

@@ -49,6 +49,23 @@ def test_coop_parity(coop, method, dtype, K):
     print(f"case path {path} {wl.name} K={K} {dtype} {method}", full_parity(lib, wl, grads=grads), flush=True)
 
 
+@pytest.mark.parametrize("method", ["mgda", "pcgrad", "cagrad", "mean"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("K", [5, 6, 7, 8])
+def test_hybrid_parity_more_tasks(gpu_lib, method, dtype, K):
+    """The pipelined kernel for K = 5..8 (one or two kept register vectors,
+    one LDS vector, one or two streamed per step)."""
+    gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
+    try:
+        wl = small_workload(BASE, sum(LENS), bucket_lens=LENS, K=K, dtype=dtype, method=method,
+                            seed=9100 + 10 * K + (dtype == "bf16"))
+        grads, _, _ = to_device_inputs(wl)
+        assert gpu_lib.resolve_path(grads, wl.B + 1, method) == gpu_lib.PATH_HYBRID
+        print(f"case hybrid {wl.name} K={K} {dtype} {method}", full_parity(gpu_lib, wl, grads=grads), flush=True)
+    finally:
+        gpu_lib.set_resolve_path(0)
+
+
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_coop_output_types(coop, out_dtype):
     lib, path = coop
