@@ -86,12 +86,13 @@ def test_row_layouts(gpu_lib, dtype, layout):
     print(full_parity(gpu_lib, wl, grads=rows), flush=True)
 
 
-@pytest.mark.parametrize("path", ["PATH_TWO_PASS", "PATH_RESIDENT", "PATH_HYBRID"])
-def test_in_place_update(gpu_lib, path):
+@pytest.mark.parametrize("path,K", [("PATH_TWO_PASS", 4), ("PATH_RESIDENT", 4), ("PATH_HYBRID", 4),
+                                    ("PATH_HYBRID", 6), ("PATH_HYBRID", 8)])
+def test_in_place_update(gpu_lib, path, K):
     """The update written over one of the gradient rows equals the
     out-of-place update of the same path bitwise (every position is read
     before it is written, on each path)."""
-    wl = small_workload(BASE, 350_008, bucket_lens=[20_000, 130_000, 1, 200_007], K=4, dtype="bf16", seed=4)
+    wl = small_workload(BASE, 350_008, bucket_lens=[20_000, 130_000, 1, 200_007], K=K, dtype="bf16", seed=4)
     g = fill_grads(wl, device="cuda")
     offs = torch.from_numpy(wl.offsets()).cuda()
     gpu_lib.set_resolve_path(getattr(gpu_lib, path))
