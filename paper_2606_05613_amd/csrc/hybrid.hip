@@ -1,6 +1,7 @@
 // Pipelined, partly resident resolve: one cooperative kernel in which the
 // Gram pass of bucket b+1 runs while the weights of bucket b are computed,
-// and each bucket is half held on chip between its Gram pass and its combine.
+// and part of each bucket (about half at K <= 4) is held on chip between its
+// Gram pass and its combine.
 //
 // Why.  The two-pass path reads every gradient twice, (2K+1)*s*N bytes.  The
 // single-read kernel holds a whole bucket on chip (a 25 MiB K=4 bf16 bucket
@@ -11,18 +12,18 @@
 // produced, and bucket b's combine re-reads only the part it did not keep.
 //
 // How.  K <= 8.  Workgroups of 256 threads, two per CU (two can sit in
-// different phases, so one computes while the other streams).  The first kHybSolvers
-// workgroups of the grid hold no data: solver j
-// takes buckets j, j + kHybSolvers, ...; it waits until every data workgroup
+// different phases, so one computes while the other streams).  The first
+// kHybSolvers workgroups of the grid hold no data: solver j takes buckets
+// j, j + kHybSolvers, ...; it waits until every data workgroup
 // has stored its partial Gram of the bucket, adds the partials in a fixed
 // order, solves on one wavefront and publishes the weights with a flag.  A
 // data workgroup w owns the w-th of at most GD segments of every bucket
 // (GD data workgroups; segments are whole multiples of one vector per
 // thread; equal, or longer for the workgroups dispatched first onto their
 // CU when the host asks for a skew, see hybrid_segment).  Of its segment it
-// keeps the first NB = NR + NL vectors per task
-// row and thread in one of two buffers (registers and LDS) and streams the
-// rest.  Per workgroup the order is
+// keeps the first NB = NR + NL vectors per task row and thread in one of two
+// buffers (registers and LDS) and streams the rest, NS vectors per row at a
+// time (hyb_regs, hyb_lds, hyb_stream).  Per workgroup the order is
 //   Gram(0) -> A, Gram(1) -> B, Combine(0) <- A, Gram(2) -> A, Combine(1) <- B, ...
 // A Gram phase computes the segment's partial Gram (the same fp32 arithmetic
 // and fixed-order reductions as the streaming pass), stores it in the
