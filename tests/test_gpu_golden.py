@@ -81,6 +81,8 @@ def test_golden_tiled(gpu_lib, case, dtype, path):
     m = _method(case)
     g = torch.tensor(case["g"], dtype=torch.float64, device=dev)
     K, dim = g.shape
+    if path == "resident" and K > 4:
+        pytest.skip("the resident kernel runs K <= 4")
     reps = TILE_BUCKET // dim * TILE_B
     grads = g.repeat(1, reps).to(torch.float32 if dtype == "f32" else torch.bfloat16).contiguous()
     offs = torch.arange(TILE_B + 1, dtype=torch.int64, device=dev) * TILE_BUCKET

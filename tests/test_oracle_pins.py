@@ -630,12 +630,12 @@ def _golden(*prefixes):
 
 def check_mgda_fw_k3(fw_fn):
     # the hand-derived three- and four-task Frank-Wolfe runs
-    for c, G in _golden("mgda3", "mgda4"):
+    for c, G in _golden("mgda3", "mgda4", "mgda8"):
         np.testing.assert_allclose(fw_fn(G, 20), c["alpha"], rtol=0, atol=1e-12)
 
 
 def check_cagrad_fw_k3(ca_fn):
-    for c, G in _golden("cagrad3", "cagrad4", "cagrad_vertex"):
+    for c, G in _golden("cagrad3", "cagrad4", "cagrad8", "cagrad_vertex"):
         np.testing.assert_allclose(ca_fn(G, c["c"], 20)[0], c["weights"], rtol=0, atol=1e-12)
 
 
