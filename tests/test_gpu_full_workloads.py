@@ -4,8 +4,10 @@ configuration the benchmark times (automatic grid).
 At these sizes the oracle cannot redo everything, so each workload checks:
 * every bucket: the oracle's solver run on the GPU's own Gram matrix
   (stage-isolated weights and method variable) and simplex feasibility;
-* sampled buckets (first, last and two seeded others): the oracle's Gram,
-  its end-to-end weights and the update, as in the small-size tests;
+* sampled buckets (first, last and fourteen seeded others, plus four seeded
+  conflict buckets where the workload plants a strongly negative pair): the
+  oracle's Gram, its end-to-end weights and the update, as in the
+  small-size tests;
 * 100k seeded element positions spread over all N: the update element
   against the exactly computed weighted sum of the GPU weights (bf16 output:
   the correctly rounded value; fp32 output: within K fp32 ulps of the sum
@@ -42,7 +44,30 @@ def _free():
     torch.cuda.empty_cache()
 
 
-def _check_workload(lib, wl, grads, offs, order):
+N_SAMPLED = 16      # buckets checked end to end per workload
+N_CONFLICT = 4      # of which drawn with a strongly negative pair, where the workload has them
+
+
+def _sampled_buckets(wl):
+    """First, last and seeded others, up to N_SAMPLED; for a workload whose
+    recipe plants a strongly negative pair in some buckets, N_CONFLICT of
+    those as well (they define the K=8 CAGrad workload)."""
+    rng = np.random.default_rng(wl.seed)
+    picks = {0, wl.B - 1}
+    if wl.corr.kind == "conflict":
+        C = wl.correlations()
+        iu = np.triu_indices(wl.K, 1)
+        conflict = np.flatnonzero(C[:, iu[0], iu[1]].min(axis=1) <= 0.5 * wl.corr.c_hi)
+        picks |= set(rng.choice(conflict, size=min(N_CONFLICT, len(conflict)), replace=False).tolist())
+    rest = np.setdiff1d(np.arange(wl.B), sorted(picks))
+    picks |= set(rng.choice(rest, size=min(max(N_SAMPLED - len(picks), 0), len(rest)),
+                            replace=False).tolist())
+    return sorted(picks), rng
+
+
+def _check_workload(lib, wl, grads, offs, order, gram_cache=None):
+    """gram_cache: bucket -> the oracle's Gram of that bucket, shared by calls
+    on the same gradients (the methods of one bucket-size sweep)."""
     print(f"case {wl.name}: K={wl.K} N={wl.N} B={wl.B} {wl.dtype} {wl.method}", flush=True)
     res = run_resolve(lib, wl, grads, offs, order)
     orders_np = wl.orders() if wl.method == "pcgrad" else None
@@ -97,14 +122,19 @@ def _check_workload(lib, wl, grads, offs, order):
               flush=True)
     # sampled buckets end to end
     offs_np = wl.offsets()
-    rng = np.random.default_rng(wl.seed)
-    picks = sorted({0, wl.B - 1, *rng.choice(wl.B, size=min(2, wl.B), replace=False).tolist()})
+    picks, rng = _sampled_buckets(wl)
+    if gram_cache is None:
+        gram_cache = {}
     for b in picks:
         lo, hi = int(offs_np[b]), int(offs_np[b + 1])
         rows = host_rows(grads, lo, hi)
         ob = np.array([0, hi - lo])
-        ora = oracle.resolve(rows, ob, wl.method, max_iter=wl.max_iter, cagrad_c=wl.cagrad_c,
-                             orders=None if orders_np is None else orders_np[b:b + 1])
+        x64 = oracle.decode_rows(rows)
+        if b not in gram_cache:
+            gram_cache[b] = oracle.gram(x64, ob)
+        ora = {"gram": gram_cache[b]}
+        ora["weights"], _ = oracle.solve(ora["gram"], wl.method, wl.max_iter, wl.cagrad_c,
+                                         None if orders_np is None else orders_np[b:b + 1])
         assert_gram(res["gram"][b:b + 1], ora["gram"], wl.dtype, f"{wl.name} bucket {b}")
         tau = TAU[wl.dtype]
         assert_conflicts([c[b:b + 1] for c in conf], oracle.conflicts(ora["gram"]),
@@ -116,9 +146,9 @@ def _check_workload(lib, wl, grads, offs, order):
         out_b = res["out"][lo:hi].cpu()
         store = out_b.view(torch.int16).numpy().view(np.uint16) if out_b.dtype == torch.bfloat16 \
             else out_b.numpy()
-        assert_out(store, oracle.decode_rows(rows), ob, res["weights"][b:b + 1], ora["weights"], wl.dtype,
+        assert_out(store, x64, ob, res["weights"][b:b + 1], ora["weights"], wl.dtype,
                    where=f"{wl.name} bucket {b}")
-        del rows, ora
+        del rows, x64, ora
     # sampled elements over all of N
     idx_np = np.sort(rng.choice(wl.N, size=100_000, replace=False)).astype(np.int64)
     idx = torch.from_numpy(idx_np).to(grads.device)
@@ -172,10 +202,11 @@ def test_full_qwen_k10_bucket_sweep(gpu_lib, mib):
     grads = fill_grads(base, device="cuda")
     offs = torch.from_numpy(base.offsets()).cuda()
     try:
+        grams = {}
         for m in ("mgda", "pcgrad", "cagrad"):
             wl = WORKLOADS[f"qwen-1.7b-k10-{mib}mib-{m}-f32"]
             order = torch.from_numpy(wl.orders()).cuda() if m == "pcgrad" else None
-            _check_workload(gpu_lib, wl, grads, offs, order)
+            _check_workload(gpu_lib, wl, grads, offs, order, grams)
     finally:
         del grads
         _free()

@@ -3,7 +3,8 @@
 Each example's Gram matrix goes through the solve entry point and its task
 gradients (one bucket) through the whole resolve, against the values
 derived by hand from the method's definitions (Eq. mgda, Eq. pcgrad_proj
-with Algorithm 1, Eq. cagrad).  The Gram matrices of these vectors are
+with Algorithm 1, Eq. cagrad), each after the number of solver iterations
+the case states (20 unless given).  The Gram matrices of these vectors are
 exact in floating point (small integers), so the only error allowed is the
 fp32 rounding of the weights and of the update.
 """
@@ -38,10 +39,13 @@ def test_golden_solve(case):
     g = np.array(case["g"], dtype=np.float64)
     G = torch.from_numpy((g @ g.T)[None].copy()).to(dev)
     m = _method(case)
-    w, _ = bkmoo.solve(G, m, 20, case.get("c", 0.5), _order(case, dev))
+    w, aux = bkmoo.solve(G, m, case.get("iters", 20), case.get("c", 0.5), _order(case, dev))
     want = np.array(case["alpha"] if m == "mgda" else case["weights"])
     got = w.cpu().numpy()[0].astype(np.float64)
     assert np.all(np.abs(got - want) <= 1e-6 * np.maximum(1.0, np.abs(want))), (case["name"], got, want)
+    if "w" in case:   # the CAGrad dual variable after the case's iterations
+        got_w = aux.cpu().numpy()[0]
+        assert np.all(np.abs(got_w - np.array(case["w"])) <= 1e-12), (case["name"], got_w)
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c["name"] for c in CASES])
@@ -51,7 +55,8 @@ def test_golden_resolve(case):
     g = torch.tensor(case["g"], dtype=torch.float32, device=dev)
     n = g.shape[1]
     offs = torch.tensor([0, n], dtype=torch.int64, device=dev)
-    out = bkmoo.resolve(g.contiguous(), offs, _method(case), 20, case.get("c", 0.5), _order(case, dev))
+    out = bkmoo.resolve(g.contiguous(), offs, _method(case), case.get("iters", 20), case.get("c", 0.5),
+                        _order(case, dev))
     torch.cuda.synchronize()
     got = out.cpu().numpy().astype(np.float64)
     want = np.array(case["d"])
@@ -92,8 +97,8 @@ def test_golden_tiled(gpu_lib, case, dtype, path):
     W = torch.empty((TILE_B, K), dtype=torch.float32, device=dev)
     lib.set_resolve_path(p)
     try:
-        assert lib.resolve_path(grads, TILE_B + 1, m) == p
-        out = lib.resolve(grads, offs, m, 20, case.get("c", 0.5), order, weights=W)
+        assert lib.resolve_path(grads, TILE_B + 1, m, case.get("iters", 20)) == p
+        out = lib.resolve(grads, offs, m, case.get("iters", 20), case.get("c", 0.5), order, weights=W)
         torch.cuda.synchronize()
     finally:
         lib.set_resolve_path(0)

@@ -179,9 +179,14 @@ def test_golden_hand_examples():
             np.testing.assert_allclose(w, c["weights"], atol=1e-12)
             np.testing.assert_allclose(w @ g, c["d"], atol=1e-12)
         elif c["name"].startswith("cagrad"):
-            for w, _ in (oracle.cagrad_fw(G, c["c"], 20), oracle.cagrad_exact(G, c["c"])):
-                np.testing.assert_allclose(w, c["weights"], atol=1e-9)
-                np.testing.assert_allclose(w @ g, c["d"], atol=1e-9)
+            runs = [oracle.cagrad_fw(G, c["c"], c.get("iters", 20))]
+            if c.get("iters", 20) == 20:
+                runs.append(oracle.cagrad_exact(G, c["c"]))    # the cases at 20 steps are optima
+            for wts, w in runs:
+                np.testing.assert_allclose(wts, c["weights"], atol=1e-9)
+                np.testing.assert_allclose(wts @ g, c["d"], atol=1e-9)
+                if "w" in c:
+                    np.testing.assert_allclose(w, c["w"], atol=1e-12)
 
 
 def _simplex_grid(k, step):
@@ -635,8 +640,48 @@ def check_mgda_fw_k3(fw_fn):
 
 
 def check_cagrad_fw_k3(ca_fn):
+    # the hand-derived runs: symmetric optima, an asymmetric optimum reached by
+    # the first step, and the first two steps of an asymmetric run
     for c, G in _golden("cagrad3", "cagrad4", "cagrad8", "cagrad_vertex"):
-        np.testing.assert_allclose(ca_fn(G, c["c"], 20)[0], c["weights"], rtol=0, atol=1e-12)
+        wts, w = ca_fn(G, c["c"], c.get("iters", 20))
+        np.testing.assert_allclose(wts, c["weights"], rtol=0, atol=1e-12)
+        if "w" in c:
+            np.testing.assert_allclose(w, c["w"], rtol=0, atol=1e-12)
+
+
+def _cagrad_dual(G, c, w):
+    """F(w) = <g_w, g_avg> + c |g_avg| |g_w| from the vectors' Gram matrix:
+    <g_w, g_avg> = w^T G 1 / K and |g|^2 = the quadratic forms."""
+    k = G.shape[0]
+    one = np.full(k, 1.0 / k)
+    return float(w @ G @ one) + c * math.sqrt(max(float(one @ G @ one), 0.0)) * math.sqrt(max(float(w @ G @ w), 0.0))
+
+
+def check_cagrad_fw_descent(ca_fn):
+    """Frank-Wolfe with an exact line search never raises the dual objective,
+    stays on the simplex and approaches the exact minimiser (whose optimality
+    is pinned by the trust-region, duality-gap and grid checks above)."""
+    for k in (3, 4, 6, 8, 10):
+        rng = np.random.default_rng(700 + k)
+        for trial in range(3):
+            n = 64
+            x = rand_grads(rng, k, n, corr=rand_corr(rng, k, -0.7, 0.7),
+                           scales=np.exp(rng.uniform(-1, 1, size=k)))
+            G = x @ x.T
+            scale = float(np.max(np.diag(G)))
+            for c in (0.25, 0.5, 0.9):
+                f_opt = _cagrad_dual(G, c, oracle.cagrad_exact(G, c)[1])
+                prev = math.inf
+                for it in (0, 1, 2, 5, 20, 100):
+                    w = ca_fn(G, c, it)[1]
+                    assert w.min() >= 0 and abs(w.sum() - 1) <= 1e-12
+                    f = _cagrad_dual(G, c, w)
+                    assert f <= prev + 1e-12 * scale
+                    prev = f
+                f0 = _cagrad_dual(G, c, np.full(k, 1.0 / k))
+                f_long = _cagrad_dual(G, c, ca_fn(G, c, 2000)[1])
+                assert f_opt - 1e-12 * scale <= f_long <= f_opt + 1e-3 * scale
+                assert f_long - f_opt <= 0.01 * (f0 - f_opt) + 1e-12 * scale
 
 
 def check_pcgrad(pc_fn):
@@ -682,6 +727,9 @@ def test_checks_pass_on_the_oracle():
     check_mgda_fw_k3(oracle.mgda_fw)
     check_mgda_fw_k3(_fw_copy())
     check_cagrad_fw_k3(oracle.cagrad_fw)
+    check_cagrad_fw_k3(_cagrad_fw_copy())
+    check_cagrad_fw_descent(oracle.cagrad_fw)
+    check_cagrad_fw_descent(_cagrad_fw_copy())
     check_conflicts(oracle.conflicts)
     check_slice_offsets(oracle.slice_offsets)
     check_gram_reduce(oracle.gram_reduce)
@@ -745,6 +793,46 @@ def _cagrad_fw_argmax(G, c, iters):
         return ref.cagrad_fw(G, c, iters)
     finally:
         ref.np = good
+
+
+def _cagrad_fw_copy(start=None, full_gradient=True, step_on_vertex=True):
+    """The oracle's CAGrad Frank-Wolfe, restated so one step can be changed:
+    the start point, the gradient's second term r G w/|g_w|, and which end of
+    the segment the line-search variable weights."""
+    def fw(G, c, iters):
+        k = G.shape[0]
+        b = G.sum(axis=1) / k
+        r = c * math.sqrt(max(float(G.sum()) / (k * k), 0.0))
+        w = np.full(k, 1.0 / k) if start is None else np.eye(k)[start]
+        for _ in range(iters):
+            gw = G @ w
+            cq = float(w @ gw)
+            nrm = math.sqrt(max(cq, 0.0))
+            grad = b + (r * gw / nrm if (nrm > 1e-300 and full_gradient) else 0.0)
+            s = int(np.argmin(grad))
+            bw = float(b @ w)
+            beta1 = float(b[s]) - bw
+            A = float(G[s, s]) - 2.0 * float(gw[s]) + cq
+            Bq = float(gw[s]) - cq
+            cands = [0.0, 1.0]
+            D = r * r * A - beta1 * beta1
+            if A > 0.0 and D > 0.0 and (A * cq - Bq * Bq) / D >= 0.0:
+                root = abs(beta1) * math.sqrt((A * cq - Bq * Bq) / D)
+                cands += [g for g in ((-Bq - root) / A, (-Bq + root) / A) if 0.0 < g < 1.0]
+            cands.sort()
+            vals = [bw + beta1 * g + r * math.sqrt(max(A * g * g + 2.0 * Bq * g + cq, 0.0)) for g in cands]
+            gamma = cands[int(np.argmin(vals))]
+            if step_on_vertex:
+                w = (1.0 - gamma) * w
+                w[s] += gamma
+            else:
+                w = gamma * w
+                w[s] += 1.0 - gamma
+        nrm = math.sqrt(max(float(w @ G @ w), 0.0))
+        if r == 0.0 or nrm <= 1e-12 * math.sqrt(max(float(np.max(np.diag(G))), 0.0)):
+            return np.full(k, 1.0 / k), w
+        return 1.0 / k + (r / nrm) * w, w
+    return fw
 
 
 def _pcgrad_projects_off_current(G, order):
@@ -841,6 +929,10 @@ def _gram_reduce_drops_last(parts):
     (check_mgda_fw_k3, _fw_copy(vertex=np.argmax)),
     (check_mgda_fw_k3, _fw_copy(line=lambda aa, ab, bb: (bb, ab, aa))),
     (check_cagrad_fw_k3, _cagrad_fw_argmax),
+    (check_cagrad_fw_k3, _cagrad_fw_copy(start=0)),
+    (check_cagrad_fw_k3, _cagrad_fw_copy(full_gradient=False)),
+    (check_cagrad_fw_k3, _cagrad_fw_copy(step_on_vertex=False)),
+    (check_cagrad_fw_descent, _cagrad_fw_copy(full_gradient=False)),
     (check_pcgrad, _pcgrad_projects_off_current),
     (check_pcgrad, _pcgrad_sign_flip),
     (check_cagrad, _cagrad_radius_squared),
