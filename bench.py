@@ -5,9 +5,8 @@
 A step is one pass of the whole hot path over the workload's gradients,
 already resident in HBM: the per-bucket Gram matrices, the per-bucket solve
 and the combined update.  The step runs what bkmoo_resolve runs for the
-workload: one of its cooperative kernels (the pipelined, partly resident
-one or the single-read one) when it takes one, as one call, else the
-two-pass kernels through the three stage entry points in stream order
+workload: its cooperative kernel (the pipelined, partly resident one) when
+it takes that path, as one call, else the two-pass kernels through the three stage entry points in stream order
 (identical results to bkmoo_resolve's two-pass path, and each stage can be
 timed).  The default workload is the Llama-3-8B-shaped K=4 bf16 MGDA
 (Frank-Wolfe, 20 iterations) case with 25 MiB buckets.  Prints ONE JSON
@@ -23,13 +22,20 @@ Reported next to the throughput:
                K*s*N + s_out*N and gets no credit for its re-reads, part of
                which the last-level cache serves (`requested_frac`: the
                bytes it does request, re-reads included, per launch
-               duration, over 8 TB/s).  `traffic` (HBM bytes per launch)
-               comes from the committed rocprofv3 counter summary when it
-               matches the current kernel source, else null;
+               duration, over 8 TB/s).  `traffic` (bytes per launch) comes
+               from the committed rocprofv3 counter summary (FETCH_SIZE +
+               WRITE_SIZE, scaled by a copy kernel's reading) when it
+               matches the current kernel source, else null.  These counters
+               sit between the L2 and the fabric: on gfx950 no counter
+               separates Infinity Cache hits from DRAM, so for a kernel that
+               re-reads (the cooperative one) `traffic` is an upper bound of
+               its DRAM bytes and the one-read floor a lower bound
+               (`traffic_kind`, `dram_bytes_bounds`);
   two_pass     when the step ran a cooperative kernel: the plain two-pass
                resolve on the same inputs, with its (2K+1)*s*N bytes;
   cpu_baseline the float64 oracle on a bounded prefix of the same buckets,
-               on this host's cores (count and model).
+               one bucket per worker thread over this host's cores (count
+               and model).
 """
 
 from __future__ import annotations
@@ -60,8 +66,6 @@ def log(msg):
 KERNEL_SOURCES = {
     "gram": ["gram.hip", "stream_common.h", "internal.h"],
     "combine": ["combine.hip", "combine_impl.h", "stream_common.h", "internal.h"],
-    "resident": ["resident.hip", "coop_common.h", "combine_impl.h", "solve_impl.h", "stream_common.h",
-                 "internal.h"],
     "hybrid": ["hybrid.hip", "coop_common.h", "combine_impl.h", "solve_impl.h", "stream_common.h",
                "internal.h"],
 }
@@ -78,50 +82,68 @@ def kernel_source_sha(kernel: str) -> str:
 
 
 def committed_traffic(workload: str, kernel: str):
-    """HBM bytes per launch of `kernel` on `workload` from the committed
-    rocprofv3 counter summary, if it was taken on the current source."""
+    """Bytes per launch of `kernel` on `workload` between the L2 and the
+    fabric (FETCH_SIZE + WRITE_SIZE, calibrated) from the committed rocprofv3
+    counter summary, if it was taken on the current source."""
     path = os.path.join(PROFILE_DIR, f"{kernel}_{workload}_pmc.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     sha = re.search(r"source_sha:\s*(\w+)", text)
-    val = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    val = re.search(r"fabric_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not sha or not val or sha.group(1) != kernel_source_sha(kernel):
         return None
     return float(val.group(1))
 
 
+# worker threads of the CPU baseline: the host's cores, at most the 16 a
+# one-GPU share of the machine has
+CPU_WORKERS_MAX = 16
+
+
 def cpu_baseline(wl, grads, target_s: float):
-    """The oracle, as it stands, on a prefix of the workload's buckets."""
+    """The oracle, as it stands, on a prefix of the workload's buckets: one
+    bucket per worker thread (numpy releases the interpreter lock in its
+    array work; its BLAS is held to one thread per worker), batches of one
+    bucket per worker until about target_s of compute.  The device-to-host
+    copies of a batch are not timed."""
+    import concurrent.futures
     import numpy as np
     import oracle
     from synth import host_rows
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    except Exception:
-        cores = os.cpu_count() or 1
+    from threadpoolctl import threadpool_limits
+    workers = max(1, min(os.cpu_count() or 1, CPU_WORKERS_MAX))
     offs = wl.offsets()
     orders = wl.orders() if wl.method == "pcgrad" else None
-    done_elems, spent, nb = 0, 0.0, 0
-    while nb < wl.B and spent < target_s:
-        lo, hi = int(offs[nb]), int(offs[nb + 1])
-        rows = host_rows(grads, lo, hi)                       # D2H copy, not timed
-        t0 = time.perf_counter()
+
+    def one(b, rows):
+        lo, hi = int(offs[b]), int(offs[b + 1])
         oracle.resolve(rows, np.array([0, hi - lo]), wl.method, max_iter=wl.max_iter,
-                       cagrad_c=wl.cagrad_c, orders=None if orders is None else orders[nb:nb + 1])
-        spent += time.perf_counter() - t0
-        done_elems += hi - lo
-        nb += 1
+                       cagrad_c=wl.cagrad_c, orders=None if orders is None else orders[b:b + 1])
+
+    done_elems, spent, nb = 0, 0.0, 0
+    with threadpool_limits(limits=1), concurrent.futures.ThreadPoolExecutor(workers) as ex:
+        while nb < wl.B and spent < target_s:
+            batch = list(range(nb, min(wl.B, nb + workers)))
+            rows = [host_rows(grads, int(offs[b]), int(offs[b + 1])) for b in batch]   # not timed
+            t0 = time.perf_counter()
+            list(ex.map(one, batch, rows))
+            spent += time.perf_counter() - t0
+            done_elems += sum(int(offs[b + 1] - offs[b]) for b in batch)
+            nb = batch[-1] + 1
+            del rows
+    cores = workers
     cpu = ""
     try:
         with open("/proc/cpuinfo") as fh:
             cpu = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
     except OSError:
         pass
-    return {"value": wl.K * done_elems / spent, "unit": "elem/s", "cores": int(cores), "cpu": cpu, "kind": "oracle",
+    return {"value": wl.K * done_elems / spent, "unit": "elem/s", "cores": int(cores), "cpu": cpu,
+            "host_cpus": os.cpu_count(), "kind": "oracle",
             "sample": f"first {nb} of {wl.B} buckets ({wl.K}x{done_elems} elements), oracle.resolve "
-                      f"end to end (Gram, {wl.method}, combine, rounding), {spent:.1f} s"}
+                      f"end to end (Gram, {wl.method}, combine, rounding), one bucket per thread on "
+                      f"{cores} threads, {spent:.1f} s"}
 
 
 def main():
@@ -132,7 +154,7 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--path", choices=["auto", "two-pass", "resident", "hybrid"], default="auto",
+    ap.add_argument("--path", choices=["auto", "two-pass", "hybrid"], default="auto",
                     help="force bkmoo_resolve's implementation (default: the library's choice)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run one plain elementwise kernel that reads 2 GiB and writes "
@@ -181,13 +203,12 @@ def main():
     W = torch.empty((B, K), dtype=torch.float32, device=dev)
     A = torch.empty((B, K), dtype=torch.float64, device=dev)
     stream = torch.cuda.current_stream(dev)
-    bkmoo.set_resolve_path({"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS, "resident": bkmoo.PATH_RESIDENT,
-                            "hybrid": bkmoo.PATH_HYBRID}[args.path])
+    forced = {"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS, "hybrid": bkmoo.PATH_HYBRID}[args.path]
+    bkmoo.set_resolve_path(forced)
     path = bkmoo.resolve_path(grads, B + 1, wl.method, wl.max_iter)
-    path_name = {bkmoo.PATH_TWO_PASS: "two-pass", bkmoo.PATH_RESIDENT: "resident",
-                 bkmoo.PATH_HYBRID: "hybrid"}[path]
-    # the cooperative paths are one kernel: time the whole resolve call
-    cooperative = path in (bkmoo.PATH_RESIDENT, bkmoo.PATH_HYBRID)
+    path_name = {bkmoo.PATH_TWO_PASS: "two-pass", bkmoo.PATH_HYBRID: "hybrid"}[path]
+    # the cooperative path is one kernel: time the whole resolve call
+    cooperative = path == bkmoo.PATH_HYBRID
     traffic_bytes = bkmoo.resolve_traffic(K, wl.offsets(), wl.dtype, path, method=wl.method, max_iter=wl.max_iter)
     log(f"resolve path: {path_name}; it requests {traffic_bytes / 1e9:.2f} GB from memory per step")
 
@@ -216,7 +237,7 @@ def main():
         step()
     torch.cuda.synchronize()
     if bkmoo.read_device_error(ws) != 0:
-        raise RuntimeError("device reported invalid bucket offsets")
+        raise RuntimeError(f"device error word 0x{bkmoo.read_device_error(ws):x} after the warmup")
     log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
 
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
@@ -235,14 +256,14 @@ def main():
             st["gram"] += ev[0].elapsed_time(ev[1]) / args.steps
             st["solve"] += ev[1].elapsed_time(ev[2]) / args.steps
             st["combine"] += ev[2].elapsed_time(ev[3]) / args.steps
+    if bkmoo.read_device_error(ws) != 0:
+        raise RuntimeError(f"device error word 0x{bkmoo.read_device_error(ws):x} after the timed steps")
     log(f"{ms_step:.3f} ms/step; stages (ms) " + ", ".join(f"{k} {v:.3f}" for k, v in st.items()))
 
     # the plain two-pass resolve on the same inputs, reported beside a
     # cooperative path's figure (whose re-reads may hit the last-level cache)
     two_pass = None
     if cooperative:
-        saved = {"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS, "resident": bkmoo.PATH_RESIDENT,
-                 "hybrid": bkmoo.PATH_HYBRID}[args.path]
         bkmoo.set_resolve_path(bkmoo.PATH_TWO_PASS)
         try:
             def two_pass_step():
@@ -258,7 +279,7 @@ def main():
             e1t.record(stream)
             torch.cuda.synchronize()
         finally:
-            bkmoo.set_resolve_path(saved)
+            bkmoo.set_resolve_path(forced)
         tp_ms = e0t.elapsed_time(e1t) / reps
         tp_bytes = (2 * K + 1) * s * N
         two_pass = {"ms_per_step": round(tp_ms, 4), "value": K * N / (tp_ms / 1e3),
@@ -341,8 +362,13 @@ def main():
     achieved = kbytes / (kms / 1e3) / 1e9
     traffic = committed_traffic(wl.name, kname)
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-            "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic, "kernel": kname,
-            "algorithmic_bytes_per_launch": kbytes, "avg_launch_ms": round(kms, 4)}
+            "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
+            "traffic_kind": "L2-to-fabric bytes (FETCH_SIZE + WRITE_SIZE): Infinity Cache hits included",
+            "kernel": kname, "algorithmic_bytes_per_launch": kbytes, "avg_launch_ms": round(kms, 4)}
+    if traffic is not None:
+        # DRAM bytes lie between the bytes the kernel must move and what it
+        # drew through the fabric
+        roof["dram_bytes_bounds"] = [kbytes, max(traffic, kbytes)]
     if cooperative:
         # what the kernel draws from memory (one read, the second read of the
         # part it did not keep on chip, the update) over peak, beside the
@@ -376,6 +402,11 @@ def main():
     if not args.no_cpu_baseline:
         log(f"oracle CPU baseline, ~{args.cpu_seconds:.0f} s")
         result["cpu_baseline"] = cpu_baseline(wl, grads, args.cpu_seconds)
+    # release the device buffers and let the queued work finish before the
+    # interpreter tears down
+    del grads, out, ws, G, W, A
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     print(json.dumps(result), flush=True)
 
 

@@ -89,7 +89,8 @@ typedef enum {
 
 /* Device error word bits (bkmoo_read_device_error). */
 #define BKMOO_DEVERR_OFFSETS 0x1u /* bucket offsets rejected */
-#define BKMOO_DEVERR_TIMEOUT 0x2u /* a cooperative resolve's bounded wait expired (results invalid) */
+#define BKMOO_DEVERR_TIMEOUT 0x2u /* a bounded wait of the hybrid path expired: the update is invalid
+                                     (buckets whose wait expired get NaN weights and a NaN update) */
 
 /* Layout of T sets of per-slice partial Gram matrices (bkmoo_gram_reduce). */
 typedef enum {
@@ -97,12 +98,12 @@ typedef enum {
   BKMOO_SLICES_BUCKET_MAJOR = 1  /* partial[b][t][K][K]: bkmoo_gram over slice offsets */
 } bkmoo_slice_layout;
 
-/* How bkmoo_resolve runs the step (bkmoo_resolve_path). */
+/* How bkmoo_resolve runs the step (bkmoo_resolve_path).  Other values are
+ * rejected. */
 typedef enum {
   BKMOO_PATH_TWO_PASS = 1, /* Gram pass, solve, combine pass: reads the gradients twice */
-  BKMOO_PATH_RESIDENT = 2, /* one cooperative kernel, each bucket held on chip: reads them once */
-  BKMOO_PATH_HYBRID = 3    /* one cooperative kernel, half of each bucket held on chip, the next
-                              bucket's Gram overlapping this one's solve: ~(1.5K+1) reads */
+  BKMOO_PATH_HYBRID = 3    /* one cooperative kernel, part of each bucket held on chip, the next
+                              bucket's Gram overlapping this one's solve */
 } bkmoo_path;
 
 /* Hyper-parameters of the solve step (host struct). */
@@ -214,7 +215,7 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  * synchronisation.  gram, weights and aux may be NULL, in which case the
  * intermediate values live in the workspace only.
  *
- * Three implementations, same definitions and tolerances:
+ * Two implementations, same definitions and tolerances:
  *   two-pass  the kernels of bkmoo_gram, bkmoo_solve and bkmoo_combine;
  *             results equal those three calls bitwise.
  *   hybrid    (K <= 8, 16-byte-phase-aligned rows and output) one
@@ -227,19 +228,16 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  *             rounding, not bitwise; they depend on the device's CU count
  *             and, for K >= 4 with MGDA or CAGrad, on the segment layout
  *             the method selects (deterministic for given arguments).
- *   resident  (K <= 4, aligned as above) one cooperative kernel keeps each
- *             bucket in registers and LDS between its Gram and its combine,
- *             so every gradient element is read from HBM once (a bucket
- *             larger than the chip holds is read twice, still correct);
- *             same agreement with the two-pass path.
+ *             Its cross-workgroup hand-off waits are bounded: if one
+ *             expires the call still completes, sets BKMOO_DEVERR_TIMEOUT in
+ *             the workspace error word, and the buckets concerned get NaN
+ *             weights and a NaN update.
  * Automatic choice: the hybrid path for at least 8 buckets of which at
  * least 10% stays on chip, averaging (all K rows) at least max(24, 6 K)
  * MiB plus 4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA
  * iteration, 0.22 K us per CAGrad iteration, 0.1 K^2 us for PCGrad, 0 for
  * the mean), so that each bucket's hand-off is amortised; else the two
- * passes.  Exact solvers never take a cooperative path.  The resident
- * kernel runs only when forced: wherever it can run the hybrid kernel is
- * faster, and below the hybrid's sizes so are the two passes.
+ * passes.  Exact solvers never take the cooperative path.
  * bkmoo_resolve_path reports the choice; bkmoo_set_resolve_path forces one.
  */
 bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
@@ -318,23 +316,20 @@ bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *c
  * memory on `path` (*bytes, host) for these bucket offsets (host array,
  * int64 [B+1]): every gradient byte each pass reads plus the update written,
  * counted from the path's own data movement.  On the hybrid path part of the
- * second read of a streamed element is served by the last-level cache, so
- * its HBM bytes are lower; on the others all of it comes from HBM:
+ * second read of a streamed element may be served by the last-level cache,
+ * so its HBM bytes can be lower:
  *   BKMOO_PATH_TWO_PASS  2*K*s*N + s_out*N
- *   BKMOO_PATH_RESIDENT  K*s*N + s_out*N, plus K*s per element of every bucket
- *                        too large for the chip (read twice)
  *   BKMOO_PATH_HYBRID    K*s*N + s_out*N, plus K*s per element a data
  *                        workgroup did not keep on chip (read twice)
  * with s, s_out the input and output element sizes.  The small per-bucket
  * terms (offsets, Gram matrices, weights, partial sums) are left out.  The
- * cooperative paths depend on the current device's CU count; the hybrid
- * path's segments also on the method and iteration count (`method`,
+ * hybrid path depends on the current device's CU count, and its segments
+ * also on the method and iteration count (`method`,
  * `max_iter`, as given to bkmoo_resolve), which decide whether the first
  * workgroup of each CU takes a longer segment.  BKMOO_EINVAL
  * for bad sizes or pointers, invalid offsets, method or iteration count, or
  * an unknown path;
- * BKMOO_EUNSUPPORTED for the resident path with K > 4 or the hybrid path
- * with K > 8; BKMOO_EHIP when the
+ * BKMOO_EUNSUPPORTED for the hybrid path with K > 8; BKMOO_EHIP when the
  * current device cannot be queried.
  */
 bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_t *offsets_host,
@@ -359,8 +354,8 @@ bkmoo_status bkmoo_set_grid_override(int32_t workgroups);
 
 /*
  * bkmoo_resolve_path — the implementation bkmoo_resolve would use for these
- * arguments on the current device (*path, host): BKMOO_PATH_TWO_PASS,
- * BKMOO_PATH_RESIDENT or BKMOO_PATH_HYBRID.  `aligned` says whether every row and the output
+ * arguments on the current device (*path, host): BKMOO_PATH_TWO_PASS or
+ * BKMOO_PATH_HYBRID.  `aligned` says whether every row and the output
  * start at the same 16-byte phase.
  */
 bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt, bkmoo_dtype out_dt,
@@ -369,15 +364,14 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
 
 /*
  * bkmoo_set_resolve_path — force bkmoo_resolve's implementation
- * (0: automatic, BKMOO_PATH_TWO_PASS, BKMOO_PATH_RESIDENT or
- * BKMOO_PATH_HYBRID when eligible: K <= 8 (resident K <= 4), aligned rows, not an exact
- * method; the resident path is taken only when forced).  Process-wide; for
- * tests and tuning.
+ * (0: automatic, BKMOO_PATH_TWO_PASS, or BKMOO_PATH_HYBRID when eligible:
+ * K <= 8, aligned rows, not an exact method).  Process-wide; for tests and
+ * tuning.  BKMOO_EINVAL for any other value.
  */
 bkmoo_status bkmoo_set_resolve_path(int32_t path);
 
 /*
- * bkmoo_set_wait_limit — polls of the cooperative paths' bounded waits (for
+ * bkmoo_set_wait_limit — polls of the hybrid path's bounded waits (for
  * a bucket's arrivals or weights) before a workgroup gives up and sets
  * BKMOO_DEVERR_TIMEOUT
  * (default 4194304, about a second or more).  Process-wide; lets tests force

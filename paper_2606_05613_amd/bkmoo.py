@@ -27,7 +27,7 @@ F32, BF16 = 0, 1
 METHODS = {"mgda": 0, "pcgrad": 1, "cagrad": 2, "mean": 3, "mgda-exact": 4, "cagrad-exact": 5}
 DEVERR_OFFSETS = 0x1
 DEVERR_TIMEOUT = 0x2
-PATH_TWO_PASS, PATH_RESIDENT, PATH_HYBRID = 1, 2, 3
+PATH_TWO_PASS, PATH_HYBRID = 1, 3
 
 
 class BkmooError(RuntimeError):
@@ -295,9 +295,15 @@ def resolve(grads: Grads, bucket_offsets: torch.Tensor, method: str, max_iter: i
             cagrad_c: float = 0.5, pcgrad_order: Optional[torch.Tensor] = None,
             out: Optional[torch.Tensor] = None, out_dtype=None,
             gram_out: Optional[torch.Tensor] = None, weights: Optional[torch.Tensor] = None,
-            aux: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+            aux: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+            check_error: bool = False):
     """Gram -> solve -> combine on the current stream.  Returns `out`; gram,
-    weights and aux are written to the tensors passed (if any)."""
+    weights and aux are written to the tensors passed (if any).
+
+    The device error word (invalid offsets, an expired wait of the hybrid
+    path) lives in the workspace: pass `workspace` and read it with
+    read_device_error(), or set check_error=True to wait for the call and
+    raise BkmooError when the word is not zero."""
     arr, dt, K, N, dev, _ = _rows(grads)
     offs = _offsets(bucket_offsets, dev)
     B = offs.numel() - 1
@@ -317,6 +323,12 @@ def resolve(grads: Grads, bucket_offsets: torch.Tensor, method: str, max_iter: i
                                   ptr(weights, (B, K), torch.float32, "weights"),
                                   ptr(aux, (B, K), torch.float64, "aux"),
                                   ws.data_ptr(), ws.numel(), _stream_ptr(dev)), "bkmoo_resolve")
+    if check_error:
+        err = read_device_error(ws)
+        if err:
+            what = [n for bit, n in ((DEVERR_OFFSETS, "invalid bucket offsets"),
+                                     (DEVERR_TIMEOUT, "a bounded wait expired")) if err & bit]
+            raise BkmooError(f"bkmoo_resolve: device error 0x{err:x} ({', '.join(what) or 'unknown'})")
     return out
 
 
@@ -335,7 +347,7 @@ def set_grid_override(workgroups: int):
 
 def resolve_path(grads: Grads, bucket_offsets_len: int, method: str = "mgda", max_iter: int = 20,
                  out_dtype=None) -> int:
-    """PATH_TWO_PASS, PATH_RESIDENT or PATH_HYBRID: what resolve() would run for these
+    """PATH_TWO_PASS or PATH_HYBRID: what resolve() would run for these
     grads and method (output assumed aligned like the rows)."""
     arr, dt, K, N, dev, rows = _rows(grads)
     B = bucket_offsets_len - 1
@@ -364,7 +376,7 @@ def resolve_traffic(K: int, bucket_offsets, dtype, path: int, out_dtype=None, me
 
 
 def set_resolve_path(path: int):
-    """0 automatic, PATH_TWO_PASS, PATH_RESIDENT or PATH_HYBRID (process-wide)."""
+    """0 automatic, PATH_TWO_PASS or PATH_HYBRID (process-wide)."""
     _check(_lib.bkmoo_set_resolve_path(int(path)), "bkmoo_set_resolve_path")
 
 

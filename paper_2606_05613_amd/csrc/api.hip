@@ -12,17 +12,8 @@ namespace bkmoo {
 namespace {
 
 std::atomic<int> g_grid_override{0};
-std::atomic<int> g_resolve_path{0};            // 0 automatic, 1 two-pass, 2 resident, 3 hybrid
-std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the cooperative paths' bounded waits
-
-// The single-read (resident) kernel is never the automatic choice: wherever
-// it can run, the pipelined kernel can too and is faster, and at the bucket
-// sizes the pipelined kernel leaves to the two passes the resident one is
-// slower still.  Measured on MI355X, bf16, mean / PCGrad: 48 buckets of
-// 10.7 MiB per row (K=4) two-pass 1.00 ms, resident 1.51-1.58, pipelined
-// 0.70-0.72; 32 x 16 MiB (K=2) 0.50 / 1.09 / 0.40; 477 x 8 MiB (K=4) 7.1 /
-// 14.2 / 5.9; at 25 MiB (K=4, 613 buckets) 24.8 / 21.8 / 17.8.  It runs when
-// forced (bkmoo_set_resolve_path).
+std::atomic<int> g_resolve_path{0};            // 0 automatic, BKMOO_PATH_TWO_PASS, BKMOO_PATH_HYBRID
+std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the cooperative path's bounded waits
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cu_count[kMaxDevices];
@@ -115,9 +106,9 @@ Carved carve(void *ws, const Layout &L) {
                 reinterpret_cast<double *>(base + L.groups), reinterpret_cast<uint32_t *>(base + L.sync)};
 }
 
-// A cooperative kernel's grid (Grid: resident_grid or hybrid_grid)
-// on the current device, computed once per device and instantiation; 0 if
-// the kernel cannot run there.
+// The cooperative kernel's grid (Grid: hybrid_grid) on the current device,
+// computed once per device and instantiation; 0 if the kernel cannot run
+// there.
 template <int (*Grid)(int, int, int)>
 int cached_grid(int K, int dt, int out_dt) {
   static std::atomic<int> cache[kMaxDevices][kHybridMaxK - 1][2][2];  // K-2, dt, out_dt: 0 unknown, -1 none
@@ -133,13 +124,6 @@ int cached_grid(int K, int dt, int out_dt) {
     c.store(g > 0 ? g : -1);
   }
   return g > 0 ? g : 0;
-}
-
-// Workgroups for the resident path when it is forced, else 0.
-int choose_resident(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters) {
-  (void)N, (void)B, (void)iters;
-  if (g_resolve_path.load() != 2 || K > 4 || !vec || is_exact(method)) return 0;
-  return cached_grid<resident_grid>(K, dt, out_dt);
 }
 
 // The pipelined, partly resident path pays when each bucket carries enough
@@ -212,13 +196,13 @@ double solve_latency_us(int method, int K, int iters) {
 int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters,
                   int64_t cap_slots) {
   const int mode = g_resolve_path.load();
-  if (mode == 1 || mode == 2 || K > kHybridMaxK || !vec || is_exact(method)) return 0;
+  if (mode == BKMOO_PATH_TWO_PASS || K > kHybridMaxK || !vec || is_exact(method)) return 0;
   const int g = cached_grid<hybrid_grid>(K, dt, out_dt);
   if (g <= 0) return 0;
   const int gd = hybrid_data_workgroups(g);
   if (2 * (int64_t)gd > cap_slots) return 0;
   if ((N / gd + 2 * 4096) * (int64_t)elem_bytes(dt) >= ((int64_t)1 << 31)) return 0;
-  if (mode == 3) return g;
+  if (mode == BKMOO_PATH_HYBRID) return g;
   const double avg_elems = (double)N / B;
   const double bucket_bytes = avg_elems * K * elem_bytes(dt);
   const double held = (double)hybrid_held_elems(K, dt) * gd / (avg_elems > 1.0 ? avg_elems : 1.0);
@@ -347,16 +331,6 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
                       hgrid, hybrid_skew_pm(K, (int)dt, (int)method, iters, N, B, hgrid), stream);
     return hip_status(e);
   }
-  const int rgrid = choose_resident(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters);
-  if (rgrid > 0) {
-    hipError_t e = launch_schedule(bucket_offsets, B, N, resident_segment_elems(K, dt), w.chunk_start,
-                                   nullptr, w.err, w.sync, 2 * (int64_t)B * kSyncStride, stream);
-    if (e != hipSuccess) return BKMOO_EHIP;
-    e = launch_resident(K, (int)dt, (int)out_dt, grads, bucket_offsets, w.chunk_start, B, shift,
-                        (int)method, iters, c, order, G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride,
-                        w.err, g_spin_limit.load(), rgrid, stream);
-    return hip_status(e);
-  }
 
   hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start,
                                  w.group_start, w.err, nullptr, 0, stream);
@@ -421,20 +395,12 @@ bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_
     *bytes = once + (uint64_t)K * s * (uint64_t)N;
     return BKMOO_OK;
   }
-  if (path != BKMOO_PATH_RESIDENT && path != BKMOO_PATH_HYBRID) return BKMOO_EINVAL;
-  if (K > (path == BKMOO_PATH_RESIDENT ? 4 : kHybridMaxK)) return BKMOO_EUNSUPPORTED;
+  if (path != BKMOO_PATH_HYBRID) return BKMOO_EINVAL;
+  if (K > kHybridMaxK) return BKMOO_EUNSUPPORTED;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return BKMOO_EHIP;
   uint64_t reread = 0;  // elements read a second time
-  if (path == BKMOO_PATH_RESIDENT) {
-    const int g = resident_grid(K, (int)dt, (int)out_dt);
-    if (g <= 0) return BKMOO_EUNSUPPORTED;
-    const int64_t seg = resident_segment_elems(K, (int)dt);
-    for (int b = 0; b < B; ++b) {  // a bucket with more segments than workgroups is read twice
-      const int64_t n = offsets_host[b + 1] - offsets_host[b];
-      if ((n + seg - 1) / seg > g) reread += (uint64_t)n;
-    }
-  } else {
+  {
     const int g = hybrid_grid(K, (int)dt, (int)out_dt);
     if (g <= 0) return BKMOO_EUNSUPPORTED;
     const int gd = hybrid_data_workgroups(g), older = hybrid_older_workgroups(g);
@@ -481,15 +447,13 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
   if (choose_hybrid(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter,
                     layout(K, N, B, dt).cap_chunks) > 0)
     *path = BKMOO_PATH_HYBRID;
-  else if (choose_resident(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter) > 0)
-    *path = BKMOO_PATH_RESIDENT;
   else
     *path = BKMOO_PATH_TWO_PASS;
   return BKMOO_OK;
 }
 
 bkmoo_status bkmoo_set_resolve_path(int32_t path) {
-  if (path < 0 || path > 3) return BKMOO_EINVAL;
+  if (path != 0 && path != BKMOO_PATH_TWO_PASS && path != BKMOO_PATH_HYBRID) return BKMOO_EINVAL;
   g_resolve_path.store(path);
   return BKMOO_OK;
 }

@@ -1,4 +1,4 @@
-// Output helpers shared by the combine kernel and the resident resolve
+// Output helpers shared by the combine kernel and the pipelined resolve
 // kernel: the weighted sum for each output type and the vector stores.
 #pragma once
 

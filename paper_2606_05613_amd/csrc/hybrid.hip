@@ -3,13 +3,14 @@
 // and part of each bucket (about half at K <= 4) is held on chip between its
 // Gram pass and its combine.
 //
-// Why.  The two-pass path reads every gradient twice, (2K+1)*s*N bytes.  The
-// single-read kernel holds a whole bucket on chip (a 25 MiB K=4 bf16 bucket
-// is ~60% of the chip's registers and LDS), so nothing else fits: every
-// workgroup idles while the bucket's Gram is reduced and its problem solved.
-// Holding about half of each workgroup's share of a bucket leaves room for two
-// buckets: the data of bucket b+1 streams in while bucket b's weights are
-// produced, and bucket b's combine re-reads only the part it did not keep.
+// Why.  The two-pass path reads every gradient twice, (2K+1)*s*N bytes.  A
+// kernel that held a whole bucket on chip (a 25 MiB K=4 bf16 bucket is ~60%
+// of the chip's registers and LDS) would leave room for nothing else: every
+// workgroup would idle while the bucket's Gram is reduced and its problem
+// solved.  Holding about half of each workgroup's share of a bucket leaves
+// room for two buckets: the data of bucket b+1 streams in while bucket b's
+// weights are produced, and bucket b's combine re-reads only the part it did
+// not keep.
 //
 // How.  K <= 8.  Workgroups of 256 threads, two per CU (two can sit in
 // different phases, so one computes while the other streams).  The first
@@ -29,7 +30,10 @@
 // and fixed-order reductions as the streaming pass), stores it in the
 // segment's slot and arrives at the bucket's counter.  A combine phase waits
 // for the bucket's flag (bounded) and writes the update from the buffer and
-// from a second read of the streamed part.  The Gram phase reads the
+// from a second read of the streamed part.  A wait that runs out sets the
+// error word's timeout bit and the bucket's weights (solver) or the
+// workgroup's copy of them (data workgroup) become NaN, so the call ends and
+// the affected update is NaN instead of silently wrong.  The Gram phase reads the
 // streamed part with the temporal cache policy, so that second read mostly
 // hits the Infinity Cache; solver waves, and data waves in a combine phase,
 // run at raised wave priority.
@@ -42,7 +46,7 @@
 // bucket b+2's partial in Gram(b+2), after its Combine(b) saw bucket b's
 // flag, which a solver sets only after it has read bucket b's partials.
 // Cross-workgroup data moves through the agent-scope primitives of
-// coop_common.h.
+// coop_common.h, each hand-off a publish point and an observe point.
 //
 // The segments depend on the number of data workgroups (and on the skew), so
 // results are reproducible on a given device but may differ in the last bits
@@ -131,7 +135,10 @@ struct Hybrid {
     double red[kHybWaves][P];
     double red2[P][NG];
     Shared S;
-    float wsh[K];
+    // the bucket's weights, one copy per buffer: Combine(b) and Combine(b+1)
+    // can follow each other with no barrier in between (no Gram(b+2) at the
+    // end), so thread 0 must not overwrite what other waves may still read
+    float wsh[2][K];
   };
 
   // Gram phase of bucket b into buffer X (reg, hs and sm.lds[X]).
@@ -219,7 +226,7 @@ struct Hybrid {
     }
     __syncthreads();
     if (t == 0) {
-      wait_vm_complete();  // the slot (written by wave 0) is out
+      publish_point();  // the slot (stored by wave 0, before the barrier) before the arrival
       __hip_atomic_fetch_add(&a.arrive[(int64_t)b * kSyncStride], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
@@ -279,9 +286,11 @@ struct Hybrid {
 #pragma unroll
     for (int i = 0; i < K; ++i) qn[i] = buf_load16(rs[i], voff, (uint32_t)(NB * T * 16));
     if (t == 0) {
-      wait_at_least(&a.flags[(int64_t)b * kSyncStride], 1u, a);
+      const bool ok = wait_at_least(&a.flags[(int64_t)b * kSyncStride], 1u, a);
+      observe_point();  // the weights after the flag
 #pragma unroll
-      for (int i = 0; i < K; ++i) sm.wsh[i] = load_agent(&a.weights[(int64_t)b * K + i]);
+      for (int i = 0; i < K; ++i)
+        sm.wsh[X][i] = ok ? load_agent(&a.weights[(int64_t)b * K + i]) : __builtin_nanf("");
     }
     __syncthreads();
     // The two workgroups of a CU drift into different phases, and the wave
@@ -290,7 +299,7 @@ struct Hybrid {
     __builtin_amdgcn_s_setprio(1);
     float wv[K];
 #pragma unroll
-    for (int i = 0; i < K; ++i) wv[i] = sm.wsh[i];
+    for (int i = 0; i < K; ++i) wv[i] = sm.wsh[X][i];
     if (has) {
       if (t < sp.nh + sp.nt) {
         const int64_t n = t < sp.nh ? lo + t : sp.hi_a + (t - sp.nh);
@@ -326,7 +335,10 @@ struct Hybrid {
     // its CU with one: its waves go first
     __builtin_amdgcn_s_setprio(3);
     for (int b = w - GD; b < a.B; b += kHybSolvers) {
-      if (t == 0) ok_sh = wait_at_least(&a.arrive[(int64_t)b * kSyncStride], (uint32_t)GD, a) ? 1 : 0;
+      if (t == 0) {
+        ok_sh = wait_at_least(&a.arrive[(int64_t)b * kSyncStride], (uint32_t)GD, a) ? 1 : 0;
+        observe_point();  // the partial slots after the arrivals (loaded after the barrier)
+      }
       __syncthreads();
       int64_t slo, shi, nseg;
       hybrid_segment(a.offs[b + 1] - a.offs[b], 0, GD, a.older, a.skew_pm, (int64_t)T * V, slo, shi, nseg);
@@ -352,6 +364,7 @@ struct Hybrid {
       if (t < P) {
         double v = 0.0;
         for (int g = 0; g < NG; ++g) v += sm.red2[t][g];
+        if (!ok_sh) v = __builtin_nan("");  // some partials may be missing
         int i = 0, rem = t;
         while (rem >= K - i) {
           rem -= K - i;
@@ -392,12 +405,22 @@ struct Hybrid {
               ax = xr[i];
             }
         }
-        if (t < K) {
-          store_agent(&a.weights[(int64_t)b * K + t], (float)wt);
-          if (a.aux) a.aux[(int64_t)b * K + t] = ax;
+        // lane i < K holds task i's weight and variable; thread 0 gathers them
+        // and publishes the weights, then the flag
+        float wk[K];
+        double xk[K];
+#pragma unroll
+        for (int i = 0; i < K; ++i) {
+          wk[i] = (float)__shfl(wt, i, kWave);
+          xk[i] = __shfl(ax, i, kWave);
         }
         if (t == 0) {
-          wait_vm_complete();  // weights (written by this wavefront) are out
+#pragma unroll
+          for (int i = 0; i < K; ++i) {
+            store_agent(&a.weights[(int64_t)b * K + i], wk[i]);
+            if (a.aux) a.aux[(int64_t)b * K + i] = xk[i];
+          }
+          publish_point();  // the weights before the flag
           store_agent(&a.flags[(int64_t)b * kSyncStride], 1u);
         }
       }

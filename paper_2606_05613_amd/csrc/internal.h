@@ -53,10 +53,10 @@ constexpr int pairs(int K) { return K * (K + 1) / 2; }
 constexpr int kFinalizeGroup = 1024;
 
 // Partial-Gram slots the workspace always has room for (the pipelined
-// cooperative kernel uses two sets, one per workgroup that holds data).
+// cooperative kernel uses two sets of one slot per workgroup that holds data).
 constexpr int64_t kCoopSlots = 1024;
 
-// The cooperative kernels' per-bucket arrival counters and flags sit 128
+// The cooperative kernel's per-bucket arrival counters and flags sit 128
 // bytes apart (one per cache line): with 4-byte neighbours, device-scope
 // atomics on one bucket's counter and polls of the next buckets' counters
 // contend for the same line (measured: 1.4 ms of a 23 ms step).
@@ -70,7 +70,7 @@ constexpr int64_t kSyncStride = 32;  // uint32 words
 //   partials            fp64  [cap][P]    cap = ceil(N / C) + B
 //   group_start         int64 [B + 1]     (prefix sum of finalize groups per bucket)
 //   groups              fp64  [gcap][P]   gcap = cap / kFinalizeGroup + B + 1
-//   sync                uint32 [2][B][kSyncStride]  cooperative paths: arrival counters, flags
+//   sync                uint32 [2][B][kSyncStride]  cooperative path: arrival counters, flags
 struct Layout {
   size_t err, chunk_start, gram, weights, partials, group_start, groups, sync, total;
   int64_t cap_chunks, cap_groups;
@@ -148,17 +148,7 @@ hipError_t launch_gram_reduce(int K, int B, int T, const double *partial, int bu
 hipError_t launch_exact_solve(int K, int B, const double *gram, int method, double c, float *weights,
                               double *aux, hipStream_t s);
 
-// Single-read resident resolve (K <= 4): elements per segment, workgroups
-// of the cooperative launch (0 if the combination cannot run resident).
-int64_t resident_segment_elems(int K, int dt);
-int resident_grid(int K, int dt, int out_dt);
-hipError_t launch_resident(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs,
-                           const int64_t *seg_start, int B, int shift, int method, int iters, double c,
-                           const int8_t *order, double *gram, float *weights, double *aux, void *out,
-                           double *partials, uint32_t *arrive, uint32_t *flags, uint32_t *err,
-                           uint32_t spin_limit, int grid, hipStream_t s);
-
-// Pipelined, partly resident resolve (K <= 4): cooperative grid (0 if the
+// Pipelined, partly resident resolve (K <= kHybridMaxK): cooperative grid (0 if the
 // combination cannot run this way), and how many of its workgroups hold data
 // (the rest solve); partials must hold 2 * data workgroups slots.
 int hybrid_grid(int K, int dt, int out_dt);

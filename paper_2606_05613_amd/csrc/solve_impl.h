@@ -1,4 +1,4 @@
-// Per-bucket MOO solvers shared by the solve kernel and the resident
+// Per-bucket MOO solvers shared by the solve kernel and the pipelined
 // resolve kernel.  Every function is called by all threads of one wavefront
 // (WaveSync) or of the workgroup (BlockSync); lanes t < K do the per-task
 // work, the scalar steps run redundantly on every lane from LDS broadcasts.

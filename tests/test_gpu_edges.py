@@ -86,8 +86,8 @@ def test_row_layouts(gpu_lib, dtype, layout):
     print(full_parity(gpu_lib, wl, grads=rows), flush=True)
 
 
-@pytest.mark.parametrize("path,K", [("PATH_TWO_PASS", 4), ("PATH_RESIDENT", 4), ("PATH_HYBRID", 4),
-                                    ("PATH_HYBRID", 6), ("PATH_HYBRID", 8)])
+@pytest.mark.parametrize("path,K", [("PATH_TWO_PASS", 4), ("PATH_HYBRID", 4), ("PATH_HYBRID", 6),
+                                    ("PATH_HYBRID", 8)])
 def test_in_place_update(gpu_lib, path, K):
     """The update written over one of the gradient rows equals the
     out-of-place update of the same path bitwise (every position is read

@@ -96,8 +96,8 @@ def test_exact_end_to_end(gpu_lib, K, method):
     print(full_parity(gpu_lib, wl), flush=True)
 
 
-def test_exact_never_takes_the_resident_path(gpu_lib):
-    gpu_lib.set_resolve_path(gpu_lib.PATH_RESIDENT)
+def test_exact_never_takes_the_cooperative_path(gpu_lib):
+    gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
     try:
         g = torch.empty((4, 1 << 26), dtype=torch.bfloat16, device="cuda")
         for m in ("mgda-exact", "cagrad-exact"):

@@ -76,18 +76,16 @@ TILE_BUCKET = 3 << 19   # elements per bucket: whole 2- and 3-element repeats, a
 TILE_B = 12
 
 
-@pytest.mark.parametrize("path", ["two-pass", "resident", "hybrid"])
+@pytest.mark.parametrize("path", ["two-pass", "hybrid"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("case", CASES, ids=[c["name"] for c in CASES])
 def test_golden_tiled(gpu_lib, case, dtype, path):
     lib = gpu_lib
     dev = torch.device("cuda", 0)
-    p = {"two-pass": lib.PATH_TWO_PASS, "resident": lib.PATH_RESIDENT, "hybrid": lib.PATH_HYBRID}[path]
+    p = {"two-pass": lib.PATH_TWO_PASS, "hybrid": lib.PATH_HYBRID}[path]
     m = _method(case)
     g = torch.tensor(case["g"], dtype=torch.float64, device=dev)
     K, dim = g.shape
-    if path == "resident" and K > 4:
-        pytest.skip("the resident kernel runs K <= 4")
     reps = TILE_BUCKET // dim * TILE_B
     grads = g.repeat(1, reps).to(torch.float32 if dtype == "f32" else torch.bfloat16).contiguous()
     offs = torch.arange(TILE_B + 1, dtype=torch.int64, device=dev) * TILE_BUCKET

@@ -1,10 +1,9 @@
-"""The two cooperative resolve kernels against the oracle: the single-read
-(resident) kernel and the pipelined, partly resident (hybrid) one.  Every
-method and input type for K = 2..4, ragged and unaligned buckets, 1 to 41
-buckets (the hybrid kernel alternates two buffers), full 25 MiB buckets
-(whose hybrid segments stream part of their data), a bucket larger than the
-chip holds, determinism, agreement with the two-pass path, and the bounded
-waits' timeout forced from the host."""
+"""The pipelined, partly resident (hybrid) resolve kernel against the
+oracle.  Every method and input type for K = 2..8, ragged and unaligned
+buckets, 1 to 41 buckets (the kernel alternates two buffers), full 25 MiB
+buckets (whose segments stream part of their data), a bucket larger than
+the chip holds, determinism, agreement with the two-pass path, and the
+bounded waits' timeout forced from the host."""
 
 import numpy as np
 import pytest
@@ -21,12 +20,11 @@ BASE = WORKLOADS["llama3-8b-k4-mgda-bf16"]
 LENS = [70_001, 1, 0, 33_333, 131_072, 7, 65_539, 40_047]
 
 
-@pytest.fixture(params=["resident", "hybrid"])
-def coop(request, gpu_lib):
-    """The library with one of the cooperative paths forced, and that path."""
-    path = {"resident": gpu_lib.PATH_RESIDENT, "hybrid": gpu_lib.PATH_HYBRID}[request.param]
-    gpu_lib.set_resolve_path(path)
-    yield gpu_lib, path
+@pytest.fixture
+def coop(gpu_lib):
+    """The library with the cooperative (hybrid) path forced, and that path."""
+    gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
+    yield gpu_lib, gpu_lib.PATH_HYBRID
     gpu_lib.set_resolve_path(0)
 
 
@@ -143,9 +141,8 @@ def test_hybrid_skewed_segments(gpu_lib, method, dtype):
 
 
 def test_coop_bucket_larger_than_chip(coop):
-    """One K=2 fp32 bucket of 14.5M elements: the resident kernel's
-    workgroups hold several segments and re-read them; the hybrid kernel's
-    segments stream most of their data."""
+    """One K=2 fp32 bucket of 14.5M elements: the segments stream most of
+    their data."""
     lib, path = coop
     wl = small_workload(WORKLOADS["k2-mgda-1m-f32"], 14_500_000, bucket_lens=[14_500_000], seed=5)
     grads, _, _ = to_device_inputs(wl)
@@ -153,7 +150,7 @@ def test_coop_bucket_larger_than_chip(coop):
     print(full_parity(lib, wl, grads=grads), flush=True)
 
 
-@pytest.mark.parametrize("path_name", ["PATH_RESIDENT", "PATH_HYBRID"])
+@pytest.mark.parametrize("path_name", ["PATH_HYBRID"])
 def test_coop_deterministic_and_close_to_two_pass(gpu_lib, path_name):
     wl = small_workload(BASE, sum(LENS), bucket_lens=LENS, K=4, dtype="bf16", method="cagrad", seed=31)
     grads, offs, order = to_device_inputs(wl)
@@ -174,19 +171,31 @@ def test_coop_deterministic_and_close_to_two_pass(gpu_lib, path_name):
 
 
 def test_coop_wait_timeout_forced_from_host(coop):
-    """A one-poll wait limit makes waiting workgroups give up at once: the
-    call still completes (no hang) and, if any wait expired, says so."""
+    """A one-poll wait limit makes waiting workgroups give up at once.  The
+    first bucket (25 MiB per task) takes every data workgroup microseconds to
+    stream, while the solver polls its arrivals right at the start, so that
+    wait expires: the call completes (no hang), the error word says so, the
+    first bucket's Gram, weights and update are NaN, and the binding's
+    checked call raises.  A normal call on the same workspace is clean."""
     lib, path = coop
-    wl = small_workload(BASE, sum(LENS), bucket_lens=LENS, K=4, dtype="bf16", seed=41)
+    lens = [13_107_200, 65_536, 65_536, 131_072]
+    wl = small_workload(BASE, sum(lens), bucket_lens=lens, K=4, dtype="bf16", method="mgda", seed=41)
     grads, offs, _ = to_device_inputs(wl)
     assert lib.resolve_path(grads, wl.B + 1, wl.method, wl.max_iter) == path
     ws = torch.empty(lib.workspace_size(wl.K, wl.N, wl.B, "bf16"), dtype=torch.uint8, device="cuda")
+    G = torch.empty((wl.B, wl.K, wl.K), dtype=torch.float64, device="cuda")
+    W = torch.empty((wl.B, wl.K), dtype=torch.float32, device="cuda")
     try:
         lib.set_wait_limit(1)
-        lib.resolve(grads, offs, "mgda", workspace=ws)
+        out = lib.resolve(grads, offs, "mgda", 20, gram_out=G, weights=W, workspace=ws)
         err = lib.read_device_error(ws)
+        with pytest.raises(lib.BkmooError, match="bounded wait"):
+            lib.resolve(grads, offs, "mgda", 20, workspace=ws, check_error=True)
     finally:
         lib.set_wait_limit(1 << 22)
-    assert err in (0, lib.DEVERR_TIMEOUT)
-    lib.resolve(grads, offs, "mgda", workspace=ws)
+    assert err & lib.DEVERR_TIMEOUT
+    assert bool(torch.isnan(G[0]).all()) and bool(torch.isnan(W[0]).all())
+    assert bool(torch.isnan(out[:lens[0]].float()).all())
+    out2 = lib.resolve(grads, offs, "mgda", 20, workspace=ws, check_error=True)
     assert lib.read_device_error(ws) == 0
+    assert not bool(torch.isnan(out2.float()).any())

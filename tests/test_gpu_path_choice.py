@@ -3,8 +3,7 @@ MI355X shapes: the hybrid path (K <= 8) needs at least 8 buckets, at least
 10% of a bucket kept on chip, and buckets (all K rows) of at least
 max(24, 6 K) MiB plus 4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA and
 0.22 K us per CAGrad iteration, 0.1 K^2 us for PCGrad); everything else
-runs the two passes.  The single-read resident kernel runs only when
-forced.  Only shapes are used (no resolve runs); the cases sit away from
+runs the two passes.  Only shapes are used (no resolve runs); the cases sit away from
 the thresholds."""
 
 import pytest
@@ -44,8 +43,7 @@ CASES_4x2G = [
 
 @pytest.mark.parametrize("B,method,iters,want", CASES_4x2G)
 def test_automatic_path(gpu_lib, rows_4x2g, B, method, iters, want):
-    names = {gpu_lib.PATH_TWO_PASS: "two-pass", gpu_lib.PATH_RESIDENT: "resident",
-             gpu_lib.PATH_HYBRID: "hybrid"}
+    names = {gpu_lib.PATH_TWO_PASS: "two-pass", gpu_lib.PATH_HYBRID: "hybrid"}
     gpu_lib.set_resolve_path(0)
     got = names[gpu_lib.resolve_path(rows_4x2g, B + 1, method, iters)]
     assert got == want, f"B={B} {method}-{iters}: {got}"
@@ -72,8 +70,7 @@ CASES_MORE_TASKS = [
 
 @pytest.mark.parametrize("K,B,method,iters,want", CASES_MORE_TASKS)
 def test_automatic_path_more_tasks(gpu_lib, K, B, method, iters, want):
-    names = {gpu_lib.PATH_TWO_PASS: "two-pass", gpu_lib.PATH_RESIDENT: "resident",
-             gpu_lib.PATH_HYBRID: "hybrid"}
+    names = {gpu_lib.PATH_TWO_PASS: "two-pass", gpu_lib.PATH_HYBRID: "hybrid"}
     g = torch.empty((K, 1 << 28), dtype=torch.bfloat16, device="cuda")
     gpu_lib.set_resolve_path(0)
     got = names[gpu_lib.resolve_path(g, B + 1, method, iters)]
@@ -108,16 +105,16 @@ def test_misaligned_rows_take_the_two_passes(gpu_lib):
     assert gpu_lib.resolve_path(rows, 9, "mean", 0) == gpu_lib.PATH_TWO_PASS
 
 
-def test_resident_only_when_forced(gpu_lib, rows_4x2g):
-    """No shape makes the automatic choice the resident kernel; forced, it
-    runs wherever it can (aligned rows, K <= 4, iterative or not)."""
-    gpu_lib.set_resolve_path(0)
-    for B in (8, 32, 48, 64, 96, 613):
-        for m, it in (("mean", 0), ("pcgrad", 0), ("mgda", 2), ("mgda", 20)):
-            assert gpu_lib.resolve_path(rows_4x2g, B + 1, m, it) != gpu_lib.PATH_RESIDENT
-    gpu_lib.set_resolve_path(gpu_lib.PATH_RESIDENT)
+def test_forced_hybrid_and_unknown_paths(gpu_lib, rows_4x2g):
+    """Forced, the hybrid path runs wherever it can (aligned rows, K <= 8,
+    iterative or not, any bucket count); a path value other than 0, 1 and 3
+    is rejected."""
+    gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
     try:
         for B in (4, 48, 613):
-            assert gpu_lib.resolve_path(rows_4x2g, B + 1, "mgda", 20) == gpu_lib.PATH_RESIDENT
+            assert gpu_lib.resolve_path(rows_4x2g, B + 1, "mgda", 20) == gpu_lib.PATH_HYBRID
     finally:
         gpu_lib.set_resolve_path(0)
+    for bad in (-1, 2, 4):
+        with pytest.raises(gpu_lib.BkmooError):
+            gpu_lib.set_resolve_path(bad)
