@@ -247,6 +247,35 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
                            hipStream_t stream);
 
 /*
+ * bkmoo_resolve_noalloc — bkmoo_resolve for callers that cannot allocate
+ * device memory or hand the library a workspace (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation).  Same
+ * arguments as bkmoo_resolve minus workspace/ws_bytes, same paths, results
+ * and errors; the workspace is a fixed array of the library instead:
+ *   - 96 MiB per device (file-scope device memory of the library, present
+ *     on every device the library runs on until the process ends).  A call
+ *     whose bkmoo_workspace_size(K, N, B, dt) exceeds it returns
+ *     BKMOO_EWORKSPACE before anything is queued.  The size is about
+ *     K(K+1)/2 * 8 bytes per chunk of 16-32K elements: 19 MiB for K=4 bf16
+ *     over 8.03B parameters in 25 MiB buckets, 68 MiB for K=8 at that
+ *     shape, 57 MiB for K=10 fp32 over 1.72B parameters in 1 MiB buckets.
+ *   - No allocation, free or synchronisation: the first call on a device
+ *     looks up that device's address of the array (hipGetSymbolAddress)
+ *     with that device current; every call is then launches on `stream`.
+ *   - Every call on a device shares that device's array, which keeps the
+ *     last call's contents (each call clears what must start at zero):
+ *     calls that overlap in time on one device race and give undefined
+ *     results.  Serialise them (one stream, or events).
+ *   - The device error word lives in the array and cannot be read back;
+ *     invalid offsets still make the Gram matrices NaN and a timeout of the
+ *     hybrid path still makes the affected weights and update NaN.
+ */
+bkmoo_status bkmoo_resolve_noalloc(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N,
+                                   int32_t B, const int64_t *bucket_offsets, bkmoo_method method,
+                                   const bkmoo_hparams *hp, void *out, bkmoo_dtype out_dt, double *gram,
+                                   float *weights, double *aux, hipStream_t stream);
+
+/*
  * bkmoo_slice_offsets — cut every bucket into T contiguous slices: slice t
  * of bucket b is [o_b + floor(t n_b / T), o_b + floor((t+1) n_b / T)),
  * n_b = o_{b+1} - o_b, the piece rank t of T would hold after the ranks

@@ -7,7 +7,7 @@ raises on any non-OK status.  There is no fallback: if the library is not
 built, importing this module fails.
 
 Names mirror include/bkmoo.h: workspace_size, gram, solve, combine, resolve,
-conflicts, slice_offsets, gram_reduce, resolve_path, resolve_traffic,
+resolve_noalloc, conflicts, slice_offsets, gram_reduce, resolve_path, resolve_traffic,
 read_device_error, set_resolve_path, set_wait_limit, set_grid_override,
 status_string.
 """
@@ -52,6 +52,8 @@ def _load():
         "bkmoo_combine": [i32, vpp, ctypes.c_int, i64, i32, vp, vp, vp, ctypes.c_int, vp, sz, vp],
         "bkmoo_resolve": [i32, vpp, ctypes.c_int, i64, i32, vp, ctypes.c_int, ctypes.POINTER(_Hparams),
                           vp, ctypes.c_int, vp, vp, vp, vp, sz, vp],
+        "bkmoo_resolve_noalloc": [i32, vpp, ctypes.c_int, i64, i32, vp, ctypes.c_int, ctypes.POINTER(_Hparams),
+                                  vp, ctypes.c_int, vp, vp, vp, vp],
         "bkmoo_conflicts": [i32, i32, vp, vp, vp, vp, vp],
         "bkmoo_slice_offsets": [i32, i32, vp, vp, vp],
         "bkmoo_resolve_traffic": [i32, i64, i32, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, i32, i32,
@@ -75,6 +77,7 @@ def _load():
 _lib = _load()
 
 EXPORTS = ("bkmoo_workspace_size", "bkmoo_gram", "bkmoo_solve", "bkmoo_combine", "bkmoo_resolve",
+           "bkmoo_resolve_noalloc",
            "bkmoo_conflicts", "bkmoo_slice_offsets", "bkmoo_gram_reduce", "bkmoo_resolve_traffic",
            "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
            "bkmoo_set_resolve_path", "bkmoo_set_wait_limit", "bkmoo_status_string")
@@ -329,6 +332,32 @@ def resolve(grads: Grads, bucket_offsets: torch.Tensor, method: str, max_iter: i
             what = [n for bit, n in ((DEVERR_OFFSETS, "invalid bucket offsets"),
                                      (DEVERR_TIMEOUT, "a bounded wait expired")) if err & bit]
             raise BkmooError(f"bkmoo_resolve: device error 0x{err:x} ({', '.join(what) or 'unknown'})")
+    return out
+
+
+def resolve_noalloc(grads: Grads, bucket_offsets: torch.Tensor, method: str, out: torch.Tensor,
+                    max_iter: int = 20, cagrad_c: float = 0.5, pcgrad_order: Optional[torch.Tensor] = None,
+                    gram_out: Optional[torch.Tensor] = None, weights: Optional[torch.Tensor] = None,
+                    aux: Optional[torch.Tensor] = None):
+    """resolve() on the library's own fixed device scratch (bkmoo_resolve_noalloc):
+    nothing is allocated, so `out` must be given.  Calls that overlap on one
+    device share that scratch and race.  Returns `out`."""
+    arr, dt, K, N, dev, _ = _rows(grads)
+    offs = _offsets(bucket_offsets, dev)
+    B = offs.numel() - 1
+    _tensor(out, (N,), out.dtype, dev, "out")
+    hp = _hparams(max_iter, cagrad_c, pcgrad_order, K, B, dev)
+
+    def ptr(t, shape, dtype, what):
+        return None if t is None else _tensor(t, shape, dtype, dev, what)
+
+    with torch.cuda.device(dev):
+        _check(_lib.bkmoo_resolve_noalloc(K, arr, dt, N, B, offs.data_ptr(), METHODS[method], ctypes.byref(hp),
+                                          out.data_ptr(), _dt(out),
+                                          ptr(gram_out, (B, K, K), torch.float64, "gram_out"),
+                                          ptr(weights, (B, K), torch.float32, "weights"),
+                                          ptr(aux, (B, K), torch.float64, "aux"), _stream_ptr(dev)),
+               "bkmoo_resolve_noalloc")
     return out
 
 

@@ -1,6 +1,8 @@
 // C ABI of libbkmoo: argument checks, workspace carving and stream-ordered
 // launches of schedule -> Gram -> solve -> combine.  Nothing here allocates,
 // frees or synchronises (except bkmoo_read_device_error, a diagnostic).
+// bkmoo_resolve_noalloc runs bkmoo_resolve on a fixed-size device array of
+// this file instead of a caller's workspace.
 #include <atomic>
 #include <mutex>
 
@@ -17,6 +19,28 @@ std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the cooperative path'
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cu_count[kMaxDevices];
+
+// Scratch of bkmoo_resolve_noalloc: the workspace of one resolve, up to
+// kScratchBytes.  Each device holds its own copy, from when the library's
+// code object is loaded there until the process ends.  Host code never uses
+// the array's name as an address (on the host it is only a handle for the
+// runtime): g_scratch holds each device's address of it, looked up once per
+// device with that device current.
+constexpr size_t kScratchBytes = (size_t)96 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+std::atomic<void *> g_scratch[kMaxDevices];
+
+// This device's address of `scratch` (null if it cannot be had).  Two threads
+// racing on a device's first call look it up twice and store the same value.
+void *scratch_on_current_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void *p = g_scratch[dev].load();
+  if (p) return p;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+  g_scratch[dev].store(p);
+  return p;
+}
 
 bool valid_dtype(int dt) { return dt == BKMOO_F32 || dt == BKMOO_BF16; }
 
@@ -211,6 +235,27 @@ int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
   return B >= kHybridMinBuckets && bucket_bytes >= min_bytes && held >= kHybridMinHeld ? g : 0;
 }
 
+// bkmoo_resolve's argument checks (everything but the workspace); the
+// 16-byte row phase and whether rows and output allow vector accesses.
+bkmoo_status check_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
+                           const int64_t *bucket_offsets, bkmoo_method method, const bkmoo_hparams *hp,
+                           const void *out, bkmoo_dtype out_dt, int *shift, bool *vec_in, bool *vec_out) {
+  bkmoo_status st = check_shape(K, N, B, dt);
+  if (st != BKMOO_OK) return st;
+  if ((st = check_rows(K, grads, dt, N, shift, vec_in)) != BKMOO_OK) return st;
+  *vec_out = *vec_in;
+  if ((st = check_out(K, grads, dt, N, out, out_dt, *shift, vec_out)) != BKMOO_OK) return st;
+  if ((st = check_hparams(method, hp)) != BKMOO_OK) return st;
+  if (k_unsupported(K, method)) return BKMOO_EUNSUPPORTED;
+  return bucket_offsets ? BKMOO_OK : BKMOO_EINVAL;
+}
+
+// bkmoo_resolve's work, on the workspace given (see bkmoo_resolve).
+bkmoo_status resolve_impl(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
+                          const int64_t *bucket_offsets, bkmoo_method method, const bkmoo_hparams *hp,
+                          void *out, bkmoo_dtype out_dt, double *gram, float *weights, double *aux,
+                          void *workspace, size_t ws_bytes, hipStream_t stream);
+
 }  // namespace
 
 int device_cu_count() {
@@ -301,16 +346,41 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
                            const bkmoo_hparams *hp, void *out, bkmoo_dtype out_dt, double *gram,
                            float *weights, double *aux, void *workspace, size_t ws_bytes,
                            hipStream_t stream) {
-  bkmoo_status st = check_shape(K, N, B, dt);
-  if (st != BKMOO_OK) return st;
+  return resolve_impl(K, grads, dt, N, B, bucket_offsets, method, hp, out, out_dt, gram, weights, aux,
+                      workspace, ws_bytes, stream);
+}
+
+bkmoo_status bkmoo_resolve_noalloc(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N,
+                                   int32_t B, const int64_t *bucket_offsets, bkmoo_method method,
+                                   const bkmoo_hparams *hp, void *out, bkmoo_dtype out_dt, double *gram,
+                                   float *weights, double *aux, hipStream_t stream) {
   int shift = 0;
-  bool vec_in = false;
-  if ((st = check_rows(K, grads, dt, N, &shift, &vec_in)) != BKMOO_OK) return st;
-  bool vec_out = vec_in;
-  if ((st = check_out(K, grads, dt, N, out, out_dt, shift, &vec_out)) != BKMOO_OK) return st;
-  if ((st = check_hparams(method, hp)) != BKMOO_OK) return st;
-  if (k_unsupported(K, method)) return BKMOO_EUNSUPPORTED;
-  if (!bucket_offsets || !workspace) return BKMOO_EINVAL;
+  bool vec_in = false, vec_out = false;
+  const bkmoo_status st = check_resolve(K, grads, dt, N, B, bucket_offsets, method, hp, out, out_dt, &shift,
+                                        &vec_in, &vec_out);
+  if (st != BKMOO_OK) return st;
+  if (layout(K, N, B, dt).total > kScratchBytes) return BKMOO_EWORKSPACE;
+  void *ws = scratch_on_current_device();
+  if (!ws) return BKMOO_EHIP;
+  return resolve_impl(K, grads, dt, N, B, bucket_offsets, method, hp, out, out_dt, gram, weights, aux, ws,
+                      kScratchBytes, stream);
+}
+
+}  // extern "C"
+
+namespace bkmoo {
+namespace {
+
+bkmoo_status resolve_impl(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
+                          const int64_t *bucket_offsets, bkmoo_method method, const bkmoo_hparams *hp,
+                          void *out, bkmoo_dtype out_dt, double *gram, float *weights, double *aux,
+                          void *workspace, size_t ws_bytes, hipStream_t stream) {
+  int shift = 0;
+  bool vec_in = false, vec_out = false;
+  const bkmoo_status st = check_resolve(K, grads, dt, N, B, bucket_offsets, method, hp, out, out_dt, &shift,
+                                        &vec_in, &vec_out);
+  if (st != BKMOO_OK) return st;
+  if (!workspace) return BKMOO_EINVAL;
   const Layout L = layout(K, N, B, dt);
   if (ws_bytes < L.total) return BKMOO_EWORKSPACE;
   const Carved w = carve(workspace, L);
@@ -349,6 +419,11 @@ bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, 
   a.vec = vec_out;
   return hip_status(launch_combine(a, W, out, (int)out_dt, stream));
 }
+
+}  // namespace
+}  // namespace bkmoo
+
+extern "C" {
 
 bkmoo_status bkmoo_slice_offsets(int32_t B, int32_t T, const int64_t *bucket_offsets,
                                  int64_t *slice_offsets, hipStream_t stream) {

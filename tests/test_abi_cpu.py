@@ -210,3 +210,28 @@ def test_binding_rejects_bad_tensors_on_cpu(b):
                  lambda: b.resolve(torch.zeros((2, 8)), torch.zeros(2, dtype=torch.int64), "mgda")):
         with pytest.raises(ValueError, match="GPU"):
             call()
+
+
+def test_resolve_noalloc_rejects_before_queueing(b):
+    """The no-allocation resolve checks its arguments like bkmoo_resolve, and
+    a configuration whose workspace exceeds its fixed 96 MiB scratch, before
+    it looks up the scratch or queues anything."""
+    L = b._lib
+    hp = b._Hparams(20, 0.5, None)
+    offs, out = FAKE + (64 << 20), FAKE + (80 << 20)
+    # K=16 bf16 over 2^33 elements needs far more than the scratch holds
+    assert b.workspace_size(16, 1 << 33, 1, "bf16") > 96 << 20
+    assert L.bkmoo_resolve_noalloc(16, rows(16, step=1 << 34), 1, 1 << 33, 1, offs, 0, ctypes.byref(hp),
+                                   FAKE - (32 << 30), 1, None, None, None, None) == -3
+    r = rows(4)
+    assert L.bkmoo_resolve_noalloc(1, r, 1, 4096, 2, offs, 0, ctypes.byref(hp), out, 1, None, None, None,
+                                   None) == -1                                              # K < 2
+    assert L.bkmoo_resolve_noalloc(4, None, 1, 4096, 2, offs, 0, ctypes.byref(hp), out, 1, None, None, None,
+                                   None) == -1                                              # no rows
+    assert L.bkmoo_resolve_noalloc(4, r, 1, 4096, 2, None, 0, ctypes.byref(hp), out, 1, None, None, None,
+                                   None) == -1                                              # no offsets
+    bad = b._Hparams(20, 1.5, None)
+    assert L.bkmoo_resolve_noalloc(4, r, 1, 4096, 2, offs, 2, ctypes.byref(bad), out, 1, None, None, None,
+                                   None) == -1                                              # c >= 1
+    assert L.bkmoo_resolve_noalloc(4, r, 1, 4096, 2, offs, 0, ctypes.byref(hp), FAKE + 64, 1, None, None, None,
+                                   None) == -1                                              # overlapping out
