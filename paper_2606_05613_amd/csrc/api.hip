@@ -174,21 +174,48 @@ constexpr double kHybridBaseMiBPerRow = 6.0;  // ... and at least this per row (
 constexpr double kHybridMiBPerUs = 4.0;   // per microsecond of solve latency
 constexpr double kHybridMinHeld = 0.1;    // fraction of a bucket kept on chip
 
-// Segment skew for the hybrid kernel (per mille; hybrid_segment).  The
-// workgroups dispatched second onto a CU lose the wave arbiter to the first
-// and arrive last at every bucket, so the first ones can take more data.
-// Measured on MI355X (one process, K=4 bf16): a 35% skew takes 25 MiB
-// buckets from 18.4 to 17.7 ms with MGDA FW-20 (27.4 -> 24.8 with FW-100)
-// and 16 MiB buckets 7% lower, but slows the mean method by 2-5%, 50 MiB
-// CAGrad by 5%, 100 MiB buckets by 2%, and K = 2 or 3 by 5-30% (their
-// second workgroups' segments would no longer fill what they keep on chip).
-// At K = 8 it takes 25 MiB CAGrad FW-20 buckets from 40.8 to 39.2 ms; it
-// applies from K = 4 up.
+// Estimated latency of one bucket's solve on one wavefront (microseconds):
+// 0.28 us per Frank-Wolfe iteration for MGDA and 0.9 us per dual iteration
+// for CAGrad measured at K = 4, chains growing with K; PCGrad's K(K-1)
+// projections are short.
+double solve_latency_us(int method, int K, int iters) {
+  if (method == BKMOO_MGDA) return 0.07 * K * iters;
+  if (method == BKMOO_CAGRAD) return 0.22 * K * iters;
+  if (method == BKMOO_PCGRAD) return 0.1 * K * K;
+  return 0.0;
+}
+
+// How the hybrid kernel lays out a bucket for a call with a solve.  Two
+// workgroups share each CU; the one dispatched second loses the wave
+// arbiter and arrives last at every bucket, and the four data workgroups
+// that share a CU with a solver lose it to the solve (which runs at raised
+// priority).  Two remedies: a segment skew (the first-dispatched data
+// workgroups take 35% more) and leaving the solvers' CU mates without a
+// segment.  Measured on MI355X, 25 MiB buckets per row (613), bf16, ms per
+// call, skew / mates empty / neither:
+//   K=4 MGDA FW-15 17.33 / 18.03 / 17.89, FW-20 17.45 / 17.98 / 18.36,
+//       FW-40 19.04 / 18.51 / 20.78, FW-100 25.40 / 24.55 / 27.48,
+//       CAGrad FW-5 17.51 / 17.78 / 17.92, FW-10 17.77 / 17.76 / 18.75,
+//       FW-20 19.75 / 19.10 / 20.82, MGDA FW-10 17.91 / 17.64 / 17.70
+//   K=5 MGDA FW-20 27.15 / 25.96 / 25.76, CAGrad FW-20 27.58 / 24.24 / 25.62
+//   K=6 MGDA FW-20 26.39 / 25.14 / 25.99, CAGrad FW-20 28.24 / 27.01 / 29.31
+//   K=7 MGDA FW-20 31.56 / 30.59 / 31.34, CAGrad FW-20 33.77 / 32.88 / 35.81
+//   K=8 MGDA FW-20 37.96 / 35.83 / 36.06, CAGrad FW-20 38.95 / 37.73 / 40.49
+//   K=3 CAGrad FW-20 (no skew below K=4) 15.10 mates empty / 16.66 neither
+// and no difference for the mean method, PCGrad or solves under ~3 us.  So
+// the skew is for K = 4 solves of 4-9 us, and the mates go without data for
+// every other solve of 3 us or more.  The skew also needs rows of at most
+// 32 MiB per bucket (at 50 MiB it slowed CAGrad by 5%) and second
+// workgroups whose shares still fill what they keep on chip.
 constexpr int kHybridSkewPm = 350;
 constexpr double kHybridSkewMaxRowBytes = 32.0 * (1 << 20);
+constexpr double kHybridSkewMinUs = 4.0, kHybridSkewMaxUs = 9.0;
+constexpr double kHybridLightMinUs = 3.0;
 
 int hybrid_skew_pm(int K, int dt, int method, int iters, int64_t N, int B, int grid) {
-  if (K < 4 || (method != BKMOO_MGDA && method != BKMOO_CAGRAD) || iters <= 0 || B <= 0) return 0;
+  if (K != 4 || (method != BKMOO_MGDA && method != BKMOO_CAGRAD) || iters <= 0 || B <= 0) return 0;
+  const double lat = solve_latency_us(method, K, iters);
+  if (lat < kHybridSkewMinUs || lat >= kHybridSkewMaxUs) return 0;
   const double avg = (double)N / B;
   if (avg * elem_bytes(dt) > kHybridSkewMaxRowBytes) return 0;
   const int gd = hybrid_data_workgroups(grid), older = hybrid_older_workgroups(grid);
@@ -202,15 +229,17 @@ int hybrid_skew_pm(int K, int dt, int method, int iters, int64_t N, int B, int g
   return cy >= nb ? kHybridSkewPm : 0;
 }
 
-// Estimated latency of one bucket's solve on one wavefront (microseconds):
-// 0.28 us per Frank-Wolfe iteration for MGDA and 0.9 us per dual iteration
-// for CAGrad measured at K = 4, chains growing with K; PCGrad's K(K-1)
-// projections are short.
-double solve_latency_us(int method, int K, int iters) {
-  if (method == BKMOO_MGDA) return 0.07 * K * iters;
-  if (method == BKMOO_CAGRAD) return 0.22 * K * iters;
-  if (method == BKMOO_PCGRAD) return 0.1 * K * K;
-  return 0.0;
+// The hybrid kernel's layout for one call (grid from hybrid_grid).
+HybLayout hybrid_layout(int K, int dt, int method, int iters, int64_t N, int B, int grid) {
+  HybLayout L{hybrid_data_workgroups(grid), hybrid_older_workgroups(grid), 0, 0};
+  if (L.older <= 0 || L.older + kHybridSolvers >= L.nslots) return L;
+  L.skew_pm = hybrid_skew_pm(K, dt, method, iters, N, B, grid);
+  if (L.skew_pm == 0 && (method == BKMOO_MGDA || method == BKMOO_CAGRAD) &&
+      solve_latency_us(method, K, iters) >= kHybridLightMinUs) {
+    L.light = 1;
+    L.nslots -= kHybridSolvers;
+  }
+  return L;
 }
 
 // Workgroups for the pipelined, partly resident path, or 0 when it should
@@ -398,7 +427,7 @@ bkmoo_status resolve_impl(int32_t K, const void *const *grads, bkmoo_dtype dt, i
     if (e != hipSuccess) return BKMOO_EHIP;
     e = launch_hybrid(K, (int)dt, (int)out_dt, grads, bucket_offsets, B, shift, (int)method, iters, c,
                       order, G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride, w.err, g_spin_limit.load(),
-                      hgrid, hybrid_skew_pm(K, (int)dt, (int)method, iters, N, B, hgrid), stream);
+                      hgrid, hybrid_layout(K, (int)dt, (int)method, iters, N, B, hgrid), stream);
     return hip_status(e);
   }
 
@@ -478,15 +507,14 @@ bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_
   {
     const int g = hybrid_grid(K, (int)dt, (int)out_dt);
     if (g <= 0) return BKMOO_EUNSUPPORTED;
-    const int gd = hybrid_data_workgroups(g), older = hybrid_older_workgroups(g);
-    const int skew = older > 0 ? hybrid_skew_pm(K, (int)dt, (int)method, max_iter, N, B, g) : 0;
+    const HybLayout lay = hybrid_layout(K, (int)dt, (int)method, max_iter, N, B, g);
     const int64_t unit = hybrid_unit_elems((int)dt), held = hybrid_held_elems(K, (int)dt);
     for (int b = 0; b < B; ++b) {  // each segment re-reads what it did not keep
       const int64_t n = offsets_host[b + 1] - offsets_host[b];
       int64_t lo, hi, nseg, ns;
-      hybrid_segment(n, 0, gd, older, skew, unit, lo, hi, nseg);
+      lay.segment(n, 0, unit, lo, hi, nseg);
       for (int w = 0; w < nseg; ++w) {
-        hybrid_segment(n, w, gd, older, skew, unit, lo, hi, ns);
+        lay.segment(n, w, unit, lo, hi, ns);
         if (hi - lo > held) reread += (uint64_t)(hi - lo - held);
       }
     }

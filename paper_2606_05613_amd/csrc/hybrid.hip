@@ -14,14 +14,15 @@
 //
 // How.  K <= 8.  Workgroups of 256 threads, two per CU (two can sit in
 // different phases, so one computes while the other streams).  The first
-// kHybSolvers workgroups of the grid hold no data: solver j takes buckets
-// j, j + kHybSolvers, ...; it waits until every data workgroup
+// kHybridSolvers workgroups of the grid hold no data: solver j takes buckets
+// j, j + kHybridSolvers, ...; it waits until every data workgroup
 // has stored its partial Gram of the bucket, adds the partials in a fixed
 // order, solves on one wavefront and publishes the weights with a flag.  A
-// data workgroup w owns the w-th of at most GD segments of every bucket
-// (GD data workgroups; segments are whole multiples of one vector per
-// thread; equal, or longer for the workgroups dispatched first onto their
-// CU when the host asks for a skew, see hybrid_segment).  Of its segment it
+// data workgroup owns one segment slot of every bucket, or none (the host's
+// HybLayout: GD data workgroups; segments are whole multiples of one vector
+// per thread; equal, or longer for the workgroups dispatched first onto
+// their CU when the host asks for a skew; with long solves the solvers' CU
+// mates hold no segment).  Of its segment it
 // keeps the first NB = NR + NL vectors per task row and thread in one of two
 // buffers (registers and LDS) and streams the rest, NS vectors per row at a
 // time (hyb_regs, hyb_lds, hyb_stream).  Per workgroup the order is
@@ -61,7 +62,6 @@ namespace {
 
 constexpr int kHybThreads = 256;  // two workgroups per CU
 constexpr int kHybWaves = kHybThreads / kWave;
-constexpr int kHybSolvers = 4;  // workgroups that reduce and solve, holding no data
 // Partials a solver thread loads at once: with one segment per data
 // workgroup (~508) and 25 threads per Gram entry, one round trip.
 constexpr int kHybRedBatch = 24;
@@ -94,7 +94,7 @@ struct HybArgs {
   uint32_t *flags;   // [B] at stride kSyncStride, zero at launch
   uint32_t *err;
   uint32_t spin_limit;
-  int older, skew_pm;  // segment layout (hybrid_segment)
+  HybLayout lay;      // which data workgroup holds which segment
 };
 
 // buf_load16 with the default (temporal) cache policy: the line may stay in
@@ -145,11 +145,12 @@ struct Hybrid {
   static __device__ __forceinline__ void gram(const Rows<K> &rows, const HybArgs &a, Smem &sm, int b, int w, int GD,
                               int X, u32x4 (&reg)[NR][K], float (&hs)[K]) {
     const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
+    const int slot = a.lay.slot(w);
     int64_t lo, hi, nseg;
-    hybrid_segment(a.offs[b + 1] - a.offs[b], w, GD, a.older, a.skew_pm, (int64_t)T * V, lo, hi, nseg);
+    a.lay.segment(a.offs[b + 1] - a.offs[b], slot, (int64_t)T * V, lo, hi, nseg);
     lo += a.offs[b];
     hi += a.offs[b];
-    const bool has = lo < hi;  // uniform over the workgroup
+    const bool has = lo < hi;  // uniform over the workgroup; implies slot >= 0
     float acc[P];
 #pragma unroll
     for (int p = 0; p < P; ++p) acc[p] = 0.0f;
@@ -222,7 +223,7 @@ struct Hybrid {
       double v = sm.red[0][t];
 #pragma unroll
       for (int q = 1; q < kHybWaves; ++q) v += sm.red[q][t];
-      store_agent(&a.partials[((int64_t)(b & 1) * GD + w) * P + t], v);
+      store_agent(&a.partials[((int64_t)(b & 1) * GD + slot) * P + t], v);
     }
     __syncthreads();
     if (t == 0) {
@@ -267,7 +268,7 @@ struct Hybrid {
                                  int X, const u32x4 (&reg)[NR][K], const float (&hs)[K]) {
     const int t = threadIdx.x;
     int64_t lo, hi, nseg;
-    hybrid_segment(a.offs[b + 1] - a.offs[b], w, GD, a.older, a.skew_pm, (int64_t)T * V, lo, hi, nseg);
+    a.lay.segment(a.offs[b + 1] - a.offs[b], a.lay.slot(w), (int64_t)T * V, lo, hi, nseg);
     lo += a.offs[b];
     hi += a.offs[b];
     const bool has = lo < hi;
@@ -327,21 +328,21 @@ struct Hybrid {
     __builtin_amdgcn_s_setprio(0);
   }
 
-  // Solver workgroup: buckets j, j + kHybSolvers, ... (j = w - GD).
+  // Solver workgroup: buckets j, j + kHybridSolvers, ... (j = w - GD).
   static __device__ void solve(const HybArgs &a, Smem &sm, int w, int GD) {
     const int t = threadIdx.x, wave = t / kWave;
     __shared__ int ok_sh;
     // a solve sits on the critical path of every data workgroup and shares
     // its CU with one: its waves go first
     __builtin_amdgcn_s_setprio(3);
-    for (int b = w - GD; b < a.B; b += kHybSolvers) {
+    for (int b = w - GD; b < a.B; b += kHybridSolvers) {
       if (t == 0) {
         ok_sh = wait_at_least(&a.arrive[(int64_t)b * kSyncStride], (uint32_t)GD, a) ? 1 : 0;
         observe_point();  // the partial slots after the arrivals (loaded after the barrier)
       }
       __syncthreads();
       int64_t slo, shi, nseg;
-      hybrid_segment(a.offs[b + 1] - a.offs[b], 0, GD, a.older, a.skew_pm, (int64_t)T * V, slo, shi, nseg);
+      a.lay.segment(a.offs[b + 1] - a.offs[b], 0, (int64_t)T * V, slo, shi, nseg);
       // segment slots in a fixed order: group g of entry p sums segments
       // g, g+NG, ... ascending, then entry p sums its groups ascending
       if (t < P * NG) {
@@ -435,8 +436,8 @@ __global__ __launch_bounds__(kHybThreads, 2) void hybrid_kernel(Rows<K> rows, Hy
   __shared__ typename H::Smem sm;
   // the solvers are the lowest block indices: dispatched first, they are the
   // older workgroup on their CU, which the wave arbiter favours
-  const int G = gridDim.x, GD = G - kHybSolvers;
-  const int w = (int)blockIdx.x < kHybSolvers ? GD + (int)blockIdx.x : (int)blockIdx.x - kHybSolvers;
+  const int G = gridDim.x, GD = G - kHybridSolvers;
+  const int w = (int)blockIdx.x < kHybridSolvers ? GD + (int)blockIdx.x : (int)blockIdx.x - kHybridSolvers;
   if (*a.err & kErrOffsets) {
     // the schedule rejected the offsets: NaN Gram and weights, no update
     if (w == 0) {
@@ -485,7 +486,7 @@ int hybrid_grid_t() {
   // two workgroups per CU, the layout the kernel is built for (a lighter
   // instantiation could fit three, which only adds contention)
   const int g = (occ < 2 ? occ : 2) * device_cu_count();
-  return g > 2 * kHybSolvers ? g : 0;
+  return g > 2 * kHybridSolvers ? g : 0;
 }
 
 }  // namespace
@@ -508,14 +509,14 @@ int hybrid_grid(int K, int dt, int out_dt) {
 #undef BKMOO_HYB_CASE
 }
 
-int hybrid_data_workgroups(int grid) { return grid - kHybSolvers; }
+int hybrid_data_workgroups(int grid) { return grid - kHybridSolvers; }
 
 // The dispatcher gives every CU one workgroup before it gives any a second,
 // so with two per CU the first (cu count - solvers) data workgroups are the
 // older resident of their CU.
 int hybrid_older_workgroups(int grid) {
   const int cus = device_cu_count();
-  return grid == 2 * cus && cus > kHybSolvers ? cus - kHybSolvers : 0;
+  return grid == 2 * cus && cus > kHybridSolvers ? cus - kHybridSolvers : 0;
 }
 
 int64_t hybrid_held_elems(int K, int dt) {
@@ -527,11 +528,10 @@ int64_t hybrid_unit_elems(int dt) { return (int64_t)kHybThreads * vec_elems(dt);
 hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
                          int shift, int method, int iters, double c, const int8_t *order, double *gram,
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
-                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid, int skew_pm,
-                         hipStream_t s) {
-  const int older = hybrid_older_workgroups(grid);
+                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid,
+                         const HybLayout &layout, hipStream_t s) {
   const HybArgs a{offs, B, shift, method, iters, c, order, gram, weights, aux, out,
-                  partials, arrive, flags, err, spin_limit, older, older > 0 ? skew_pm : 0};
+                  partials, arrive, flags, err, spin_limit, layout};
 #define BKMOO_HYB_CASE(k)                                                                        \
   case k:                                                                                        \
     if (dt == F32)                                                                               \

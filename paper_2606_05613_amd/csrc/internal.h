@@ -154,16 +154,18 @@ hipError_t launch_exact_solve(int K, int B, const double *gram, int method, doub
 int hybrid_grid(int K, int dt, int out_dt);
 int hybrid_data_workgroups(int grid);
 // Data workgroups dispatched first onto their CU (0 unless the grid is two
-// workgroups per CU): the ones a segment skew gives more data.
+// workgroups per CU): the ones a segment skew gives more data.  The
+// kHybridSolvers workgroups dispatched right after them are the second
+// residents of the solvers' CUs.
 int hybrid_older_workgroups(int grid);
+constexpr int kHybridSolvers = 4;  // workgroups of the hybrid grid that reduce and solve
 
-// Segment [lo, hi) (relative to the bucket start) of data workgroup w in a
-// bucket of n elements, over gd data workgroups in whole units of `unit`
-// elements, and the number nseg of non-empty segments, which are always
-// workgroups 0 .. nseg-1.  skew_pm = 0: equal shares.  Otherwise the first
-// `older` workgroups take (1 + skew_pm/1000) times an equal share (rounded
-// up) and the others split the rest evenly.  Shared by the kernel and the
-// host's traffic count.
+// Segment [lo, hi) (relative to the bucket start) of slot w in a bucket of n
+// elements, over gd segment slots in whole units of `unit` elements, and
+// the number nseg of non-empty segments, which are always slots 0 ..
+// nseg-1.  skew_pm = 0: equal shares.  Otherwise the first `older` slots
+// take (1 + skew_pm/1000) times an equal share (rounded up) and the others
+// split the rest evenly.
 __host__ __device__ inline void hybrid_segment(int64_t n, int w, int gd, int older, int skew_pm, int64_t unit,
                                                int64_t &lo, int64_t &hi, int64_t &nseg) {
   const int64_t nu = (n + unit - 1) / unit;
@@ -185,6 +187,24 @@ __host__ __device__ inline void hybrid_segment(int64_t n, int w, int gd, int old
   lo = s * unit < n ? s * unit : n;
   hi = e * unit < n ? e * unit : n;
 }
+
+// How one call spreads each bucket over the hybrid kernel's data
+// workgroups.  Data workgroup w holds segment slot(w) of nslots (none when
+// slot(w) < 0).  Without `light` the slots are the workgroups themselves;
+// with it the solvers' CU mates (the kHybridSolvers workgroups after the
+// `older` ones) hold none and leave their CU to the solve.  skew_pm as in
+// hybrid_segment.  Shared by the kernel and the host's traffic count.
+struct HybLayout {
+  int nslots, older, skew_pm, light;
+  __host__ __device__ int slot(int w) const {
+    return !light || w < older ? w : w < older + kHybridSolvers ? -1 : w - kHybridSolvers;
+  }
+  // segment of slot s (s < 0: the empty one at the bucket's end)
+  __host__ __device__ void segment(int64_t n, int s, int64_t unit, int64_t &lo, int64_t &hi,
+                                   int64_t &nseg) const {
+    hybrid_segment(n, s < 0 ? nslots : s, nslots, older, skew_pm, unit, lo, hi, nseg);
+  }
+};
 // Elements of its segment a data workgroup keeps on chip per bucket, and the
 // granule segment lengths are rounded up to.
 int64_t hybrid_held_elems(int K, int dt);
@@ -192,8 +212,8 @@ int64_t hybrid_unit_elems(int dt);
 hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
                          int shift, int method, int iters, double c, const int8_t *order, double *gram,
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
-                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid, int skew_pm,
-                         hipStream_t s);
+                         uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid,
+                         const HybLayout &layout, hipStream_t s);
 
 int device_cu_count();
 

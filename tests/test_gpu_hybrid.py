@@ -110,27 +110,19 @@ def test_coop_full_size_buckets(coop):
     print(f"case path {path} 3 x 25 MiB", full_parity(lib, wl, grads=grads), flush=True)
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-@pytest.mark.parametrize("method", ["cagrad", "mgda"])
-def test_hybrid_skewed_segments(gpu_lib, method, dtype):
-    """K=4 buckets of 19-32 MiB per row (ragged) with an MGDA or CAGrad
-    solve: the hybrid kernel gives the first workgroup of each CU a longer
-    segment (the traffic count differs from the even layout's), results
-    match the oracle and repeat bitwise."""
-    lens = [9_500_001, 13_107_200, 11_000_003, 16_777_216]
-    if dtype == "f32":
-        lens = [n // 2 + 1 for n in lens]
+def _layout_case(gpu_lib, method, dtype, seed):
+    """K=4 buckets of 19-25 MiB per row, ragged, sized so that 504 and 508
+    segment slots give different segment lengths; results match the oracle
+    and repeat bitwise on the forced hybrid path."""
+    unit = 256 * (8 if dtype == "bf16" else 4)  # one 16-byte vector per thread
+    lens = [5050 * unit + 3, 6060 * unit, 6200 * unit + 1001, 5000 * unit]
     lens[-1] += -sum(lens) % (8 if dtype == "bf16" else 4)  # rows at one 16-byte phase
-    wl = small_workload(BASE, sum(lens), bucket_lens=lens, K=4, dtype=dtype, method=method,
-                        seed=630 + (dtype == "f32"))
-    skewed = gpu_lib.resolve_traffic(4, wl.offsets(), dtype, gpu_lib.PATH_HYBRID, method=method, max_iter=20)
-    even = gpu_lib.resolve_traffic(4, wl.offsets(), dtype, gpu_lib.PATH_HYBRID, method="mean", max_iter=0)
-    assert skewed != even
+    wl = small_workload(BASE, sum(lens), bucket_lens=lens, K=4, dtype=dtype, method=method, seed=seed)
     grads, offs, order = to_device_inputs(wl)
     gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
     try:
         assert gpu_lib.resolve_path(grads, wl.B + 1, method, 20) == gpu_lib.PATH_HYBRID
-        print(f"case skewed hybrid {method}", full_parity(gpu_lib, wl, grads=grads), flush=True)
+        print(f"case layout {method} {dtype}", full_parity(gpu_lib, wl, grads=grads), flush=True)
         r1 = run_resolve(gpu_lib, wl, grads, offs, order)
         r2 = run_resolve(gpu_lib, wl, grads, offs, order)
     finally:
@@ -138,6 +130,34 @@ def test_hybrid_skewed_segments(gpu_lib, method, dtype):
     assert np.array_equal(r1["gram"], r2["gram"]) and np.array_equal(r1["weights"], r2["weights"])
     assert torch.equal(r1["out"].view(torch.int32 if dtype == "f32" else torch.int16),
                        r2["out"].view(torch.int32 if dtype == "f32" else torch.int16))
+    return wl
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_hybrid_skewed_segments(gpu_lib, dtype):
+    """MGDA FW-20 at K=4 (a solve of a few microseconds): the first
+    workgroup of each CU gets a longer segment, so the bytes requested
+    differ from the even layout's (the mean method's) and from the layout
+    that leaves the solvers' CU mates empty (MGDA FW-100)."""
+    wl = _layout_case(gpu_lib, "mgda", dtype, 630 + (dtype == "f32"))
+    traffic = lambda m, it: gpu_lib.resolve_traffic(4, wl.offsets(), dtype, gpu_lib.PATH_HYBRID, method=m,
+                                                    max_iter=it)
+    skewed, even, mates = traffic("mgda", 20), traffic("mean", 0), traffic("mgda", 100)
+    assert skewed != even and skewed != mates
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_hybrid_solver_mates_hold_no_segment(gpu_lib, dtype):
+    """CAGrad FW-20 at K=4 (a solve of ~18 us): the four data workgroups on
+    the solvers' CUs hold no segment, the others share each bucket (504
+    slots instead of 508: other segment lengths, other bytes requested than
+    the even layout's); a short MGDA solve (FW-5) keeps the even layout."""
+    wl = _layout_case(gpu_lib, "cagrad", dtype, 640 + (dtype == "f32"))
+    traffic = lambda m, it: gpu_lib.resolve_traffic(4, wl.offsets(), dtype, gpu_lib.PATH_HYBRID, method=m,
+                                                    max_iter=it)
+    mates, even = traffic("cagrad", 20), traffic("mean", 0)
+    assert mates != even
+    assert traffic("mgda", 5) == even and traffic("pcgrad", 0) == even
 
 
 def test_coop_bucket_larger_than_chip(coop):
