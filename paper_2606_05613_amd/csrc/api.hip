@@ -423,7 +423,7 @@ bkmoo_status resolve_impl(int32_t K, const void *const *grads, bkmoo_dtype dt, i
       choose_hybrid(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters, L.cap_chunks);
   if (hgrid > 0) {
     hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start,
-                                   nullptr, w.err, w.sync, 2 * (int64_t)B * kSyncStride, stream);
+                                   nullptr, w.err, w.sync, (1 + kFlagCopies) * (int64_t)B * kSyncStride, stream);
     if (e != hipSuccess) return BKMOO_EHIP;
     e = launch_hybrid(K, (int)dt, (int)out_dt, grads, bucket_offsets, B, shift, (int)method, iters, c,
                       order, G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride, w.err, g_spin_limit.load(),

@@ -45,7 +45,11 @@
 // the cooperative launch keeps every workgroup resident.  Two sets of
 // partial slots suffice (bucket b uses set b & 1): a data workgroup writes
 // bucket b+2's partial in Gram(b+2), after its Combine(b) saw bucket b's
-// flag, which a solver sets only after it has read bucket b's partials.
+// flag, which a solver sets only after it has read bucket b's partials; a
+// workgroup with no segment in bucket b skips that wait, and its slot is
+// one the solver of bucket b does not read (slots past the bucket's last
+// segment).  The solver sets kFlagCopies copies of each flag; data
+// workgroup w polls copy w % kFlagCopies.
 // Cross-workgroup data moves through the agent-scope primitives of
 // coop_common.h, each hand-off a publish point and an observe point.
 //
@@ -91,7 +95,7 @@ struct HybArgs {
   void *out;
   double *partials;  // [2][GD][P]: slot set b & 1 holds bucket b's segment partials
   uint32_t *arrive;  // [B] at stride kSyncStride, zero at launch
-  uint32_t *flags;   // [B] at stride kSyncStride, zero at launch
+  uint32_t *flags;   // [kFlagCopies][B] at stride kSyncStride, zero at launch
   uint32_t *err;
   uint32_t spin_limit;
   HybLayout lay;      // which data workgroup holds which segment
@@ -104,12 +108,17 @@ __device__ __forceinline__ u32x4 buf_load16_keep(Rsrc r, uint32_t voff, uint32_t
   return __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
 }
 
-// Bounded wait until *p reaches `target` (thread 0 only); on timeout the
-// error word gets kErrTimeout and false is returned.
+// Bounded wait until *p reaches `target` (thread 0 only), SLEEP x 64 cycles
+// between polls; on timeout the error word gets kErrTimeout and false is
+// returned.  The solvers poll their arrival counters closely (the hand-off
+// starts there); data workgroups poll the weights flags about once a
+// microsecond, which costs a waiting workgroup little against a ~30 us
+// bucket and keeps ~500 pollers off the memory channels.
+template <int SLEEP>
 __device__ bool wait_at_least(const uint32_t *p, uint32_t target, const HybArgs &a) {
   uint32_t spins = 0;
   while (load_agent(p) < target) {
-    __builtin_amdgcn_s_sleep(1);
+    __builtin_amdgcn_s_sleep(SLEEP);
     if (++spins >= a.spin_limit) {
       __hip_atomic_fetch_or(a.err, kErrTimeout, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       return false;
@@ -271,8 +280,8 @@ struct Hybrid {
     a.lay.segment(a.offs[b + 1] - a.offs[b], a.lay.slot(w), (int64_t)T * V, lo, hi, nseg);
     lo += a.offs[b];
     hi += a.offs[b];
-    const bool has = lo < hi;
-    const Split<V> sp(lo, has ? hi : lo, a.shift);
+    if (lo >= hi) return;  // no segment in this bucket: no weights needed (uniform)
+    const Split<V> sp(lo, hi, a.shift);
     Rsrc rs[K];
 #pragma unroll
     for (int i = 0; i < K; ++i)
@@ -287,7 +296,8 @@ struct Hybrid {
 #pragma unroll
     for (int i = 0; i < K; ++i) qn[i] = buf_load16(rs[i], voff, (uint32_t)(NB * T * 16));
     if (t == 0) {
-      const bool ok = wait_at_least(&a.flags[(int64_t)b * kSyncStride], 1u, a);
+      const bool ok =
+          wait_at_least<32>(&a.flags[((int64_t)(w % kFlagCopies) * a.B + b) * kSyncStride], 1u, a);
       observe_point();  // the weights after the flag
 #pragma unroll
       for (int i = 0; i < K; ++i)
@@ -301,29 +311,27 @@ struct Hybrid {
     float wv[K];
 #pragma unroll
     for (int i = 0; i < K; ++i) wv[i] = sm.wsh[X][i];
-    if (has) {
-      if (t < sp.nh + sp.nt) {
-        const int64_t n = t < sp.nh ? lo + t : sp.hi_a + (t - sp.nh);
-        store_elem<ODT>(a.out, n, wsum<K, ODT>(wv, hs));
-      }
+    if (t < sp.nh + sp.nt) {
+      const int64_t n = t < sp.nh ? lo + t : sp.hi_a + (t - sp.nh);
+      store_elem<ODT>(a.out, n, wsum<K, ODT>(wv, hs));
+    }
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        u32x4 q[K];
+    for (int j = 0; j < NB; ++j) {
+      u32x4 q[K];
 #pragma unroll
-        for (int i = 0; i < K; ++i) q[i] = j < NR ? reg[j < NR ? j : 0][i] : sm.lds[X][j < NR ? 0 : j - NR][i][t];
-        const int v = j * T + t;
-        combine_vec(wv, q, a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
-      }
-      // the re-read is the data's last use: streaming policy
-      for (int j0 = NB; j0 < nslot; ++j0) {
-        u32x4 q[K];
+      for (int i = 0; i < K; ++i) q[i] = j < NR ? reg[j < NR ? j : 0][i] : sm.lds[X][j < NR ? 0 : j - NR][i][t];
+      const int v = j * T + t;
+      combine_vec(wv, q, a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
+    }
+    // the re-read is the data's last use: streaming policy
+    for (int j0 = NB; j0 < nslot; ++j0) {
+      u32x4 q[K];
 #pragma unroll
-        for (int i = 0; i < K; ++i) q[i] = qn[i];
+      for (int i = 0; i < K; ++i) q[i] = qn[i];
 #pragma unroll
-        for (int i = 0; i < K; ++i) qn[i] = buf_load16(rs[i], voff, (uint32_t)((j0 + 1) * T * 16));
-        const int v = j0 * T + t;
-        combine_vec(wv, q, a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
-      }
+      for (int i = 0; i < K; ++i) qn[i] = buf_load16(rs[i], voff, (uint32_t)((j0 + 1) * T * 16));
+      const int v = j0 * T + t;
+      combine_vec(wv, q, a.out, sp.lo_a + (int64_t)v * V, v < sp.nv);
     }
     __builtin_amdgcn_s_setprio(0);
   }
@@ -337,7 +345,7 @@ struct Hybrid {
     __builtin_amdgcn_s_setprio(3);
     for (int b = w - GD; b < a.B; b += kHybridSolvers) {
       if (t == 0) {
-        ok_sh = wait_at_least(&a.arrive[(int64_t)b * kSyncStride], (uint32_t)GD, a) ? 1 : 0;
+        ok_sh = wait_at_least<1>(&a.arrive[(int64_t)b * kSyncStride], (uint32_t)GD, a) ? 1 : 0;
         observe_point();  // the partial slots after the arrivals (loaded after the barrier)
       }
       __syncthreads();
@@ -421,8 +429,9 @@ struct Hybrid {
             store_agent(&a.weights[(int64_t)b * K + i], wk[i]);
             if (a.aux) a.aux[(int64_t)b * K + i] = xk[i];
           }
-          publish_point();  // the weights before the flag
-          store_agent(&a.flags[(int64_t)b * kSyncStride], 1u);
+          publish_point();  // the weights before the flags
+#pragma unroll
+          for (int r = 0; r < kFlagCopies; ++r) store_agent(&a.flags[((int64_t)r * a.B + b) * kSyncStride], 1u);
         }
       }
       __syncthreads();

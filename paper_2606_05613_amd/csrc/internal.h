@@ -61,6 +61,10 @@ constexpr int64_t kCoopSlots = 1024;
 // atomics on one bucket's counter and polls of the next buckets' counters
 // contend for the same line (measured: 1.4 ms of a 23 ms step).
 constexpr int64_t kSyncStride = 32;  // uint32 words
+// Copies of each bucket's weights flag on the cooperative path: ~500 data
+// workgroups poll it, and one copy (one line, one memory channel) per
+// eighth of them keeps the polls from queueing on one channel.
+constexpr int kFlagCopies = 8;
 
 // Workspace layout (every region 256-byte aligned):
 //   [0, 256)            header: uint32 error word at byte 0
@@ -70,7 +74,8 @@ constexpr int64_t kSyncStride = 32;  // uint32 words
 //   partials            fp64  [cap][P]    cap = ceil(N / C) + B
 //   group_start         int64 [B + 1]     (prefix sum of finalize groups per bucket)
 //   groups              fp64  [gcap][P]   gcap = cap / kFinalizeGroup + B + 1
-//   sync                uint32 [2][B][kSyncStride]  cooperative path: arrival counters, flags
+//   sync                uint32 [1 + kFlagCopies][B][kSyncStride]  cooperative path: arrival
+//                       counters, then kFlagCopies copies of the flags
 struct Layout {
   size_t err, chunk_start, gram, weights, partials, group_start, groups, sync, total;
   int64_t cap_chunks, cap_groups;
@@ -93,7 +98,7 @@ inline Layout layout(int K, int64_t N, int B, int dt) {
   L.cap_groups = L.cap_chunks / kFinalizeGroup + B + 1;
   L.group_start = o;    o = align256(o + sizeof(int64_t) * (size_t)(B + 1));
   L.groups = o;         o = align256(o + sizeof(double) * (size_t)L.cap_groups * pairs(K));
-  L.sync = o;           o = align256(o + sizeof(uint32_t) * 2 * (size_t)B * kSyncStride);
+  L.sync = o;           o = align256(o + sizeof(uint32_t) * (1 + kFlagCopies) * (size_t)B * kSyncStride);
   L.total = o;
   return L;
 }
