@@ -68,6 +68,8 @@ KERNEL_SOURCES = {
     "combine": ["combine.hip", "combine_impl.h", "stream_common.h", "internal.h"],
     "hybrid": ["hybrid.hip", "coop_common.h", "combine_impl.h", "solve_impl.h", "stream_common.h",
                "internal.h"],
+    "refill": ["refill.hip", "coop_common.h", "combine_impl.h", "solve_impl.h", "stream_common.h",
+               "internal.h"],
 }
 
 
@@ -154,7 +156,7 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--path", choices=["auto", "two-pass", "hybrid"], default="auto",
+    ap.add_argument("--path", choices=["auto", "two-pass", "hybrid", "refill"], default="auto",
                     help="force bkmoo_resolve's implementation (default: the library's choice)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run one plain elementwise kernel that reads 2 GiB and writes "
@@ -203,12 +205,13 @@ def main():
     W = torch.empty((B, K), dtype=torch.float32, device=dev)
     A = torch.empty((B, K), dtype=torch.float64, device=dev)
     stream = torch.cuda.current_stream(dev)
-    forced = {"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS, "hybrid": bkmoo.PATH_HYBRID}[args.path]
+    forced = {"auto": 0, "two-pass": bkmoo.PATH_TWO_PASS, "hybrid": bkmoo.PATH_HYBRID,
+              "refill": bkmoo.PATH_REFILL}[args.path]
     bkmoo.set_resolve_path(forced)
     path = bkmoo.resolve_path(grads, B + 1, wl.method, wl.max_iter)
-    path_name = {bkmoo.PATH_TWO_PASS: "two-pass", bkmoo.PATH_HYBRID: "hybrid"}[path]
+    path_name = {bkmoo.PATH_TWO_PASS: "two-pass", bkmoo.PATH_HYBRID: "hybrid", bkmoo.PATH_REFILL: "refill"}[path]
     # the cooperative path is one kernel: time the whole resolve call
-    cooperative = path == bkmoo.PATH_HYBRID
+    cooperative = path in (bkmoo.PATH_HYBRID, bkmoo.PATH_REFILL)
     traffic_bytes = bkmoo.resolve_traffic(K, wl.offsets(), wl.dtype, path, method=wl.method, max_iter=wl.max_iter)
     log(f"resolve path: {path_name}; it requests {traffic_bytes / 1e9:.2f} GB from memory per step")
 

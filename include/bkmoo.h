@@ -102,8 +102,10 @@ typedef enum {
  * rejected. */
 typedef enum {
   BKMOO_PATH_TWO_PASS = 1, /* Gram pass, solve, combine pass: reads the gradients twice */
-  BKMOO_PATH_HYBRID = 3    /* one cooperative kernel, part of each bucket held on chip, the next
+  BKMOO_PATH_HYBRID = 3,   /* one cooperative kernel, part of each bucket held on chip, the next
                               bucket's Gram overlapping this one's solve */
+  BKMOO_PATH_REFILL = 4    /* one cooperative kernel (K <= 4), most of each bucket held on chip in
+                              one buffer refilled with the next bucket as it is combined */
 } bkmoo_path;
 
 /* Hyper-parameters of the solve step (host struct). */
@@ -407,6 +409,15 @@ bkmoo_status bkmoo_set_resolve_path(int32_t path);
  * the timeout path from the host.  0 is rejected.
  */
 bkmoo_status bkmoo_set_wait_limit(uint32_t polls);
+
+/*
+ * bkmoo_set_refill_stream — vectors of 16 bytes per task row and thread
+ * that each data workgroup of the refill path always streams instead of
+ * keeping on chip (default 4); the streamed part of two buckets is the
+ * window that hides each bucket's hand-off.  Process-wide; for tuning.
+ * Negative values are rejected.
+ */
+bkmoo_status bkmoo_set_refill_stream(int32_t vectors);
 
 /* Human-readable name of a status code (static string). */
 const char *bkmoo_status_string(bkmoo_status st);

@@ -27,7 +27,7 @@ F32, BF16 = 0, 1
 METHODS = {"mgda": 0, "pcgrad": 1, "cagrad": 2, "mean": 3, "mgda-exact": 4, "cagrad-exact": 5}
 DEVERR_OFFSETS = 0x1
 DEVERR_TIMEOUT = 0x2
-PATH_TWO_PASS, PATH_HYBRID = 1, 3
+PATH_TWO_PASS, PATH_HYBRID, PATH_REFILL = 1, 3, 4
 
 
 class BkmooError(RuntimeError):
@@ -65,6 +65,7 @@ def _load():
                                ctypes.POINTER(i32)],
         "bkmoo_set_resolve_path": [i32],
         "bkmoo_set_wait_limit": [u32],
+        "bkmoo_set_refill_stream": [i32],
         "bkmoo_status_string": [ctypes.c_int],
     }
     for name, args in sig.items():
@@ -80,7 +81,7 @@ EXPORTS = ("bkmoo_workspace_size", "bkmoo_gram", "bkmoo_solve", "bkmoo_combine",
            "bkmoo_resolve_noalloc",
            "bkmoo_conflicts", "bkmoo_slice_offsets", "bkmoo_gram_reduce", "bkmoo_resolve_traffic",
            "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
-           "bkmoo_set_resolve_path", "bkmoo_set_wait_limit", "bkmoo_status_string")
+           "bkmoo_set_resolve_path", "bkmoo_set_wait_limit", "bkmoo_set_refill_stream", "bkmoo_status_string")
 
 
 def status_string(st: int) -> str:
@@ -411,3 +412,8 @@ def set_resolve_path(path: int):
 
 def set_wait_limit(polls: int):
     _check(_lib.bkmoo_set_wait_limit(int(polls)), "bkmoo_set_wait_limit")
+
+
+def set_refill_stream(vectors: int):
+    """Vectors per row and thread the refill path always streams (process-wide)."""
+    _check(_lib.bkmoo_set_refill_stream(int(vectors)), "bkmoo_set_refill_stream")

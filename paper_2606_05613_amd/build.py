@@ -14,7 +14,7 @@ fails on either finding:
   * a vector-memory store of more than 64 bits whose data registers an
     immediately following vector instruction overwrites (the store reads its
     data over two cycles and such an overwrite corrupts the stored value);
-  * a cross-workgroup hand-off of the pipelined resolve kernel out of order:
+  * a cross-workgroup hand-off of either pipelined resolve kernel out of order:
     every publish point (an inline "s_waitcnt vmcnt(0)" marked "bkmoo
     publish") must be followed, in the same block, by the flag or counter
     update as its next vector-memory instruction, and every observe point
@@ -41,9 +41,9 @@ LIB = os.path.join(PKG, "libbkmoo.so")
 ARCH = "gfx950"
 
 SOURCES = ["api.hip", "schedule.hip", "gram.hip", "solve.hip", "solve_exact.hip", "combine.hip",
-           "hybrid.hip", "conflicts.hip", "slices.hip"]
+           "hybrid.hip", "refill.hip", "conflicts.hip", "slices.hip"]
 EXTRA = {"solve.hip": ["-ffp-contract=off"], "solve_exact.hip": ["-ffp-contract=off"],
-         "hybrid.hip": ["-ffp-contract=off"],
+         "hybrid.hip": ["-ffp-contract=off"], "refill.hip": ["-ffp-contract=off"],
          "conflicts.hip": ["-ffp-contract=off"]}
 
 
@@ -164,11 +164,12 @@ def build(jobs: int = 8) -> str:
     if bad:
         detail = "\n".join(f"{a}:{ln}: {st}  ->  {nx}" for a, ln, st, nx in bad[:20])
         raise RuntimeError(f"{len(bad)} store-data overwrite hazards in the generated code:\n{detail}")
-    hyb = os.path.join(BUILD, f"hybrid-hip-amdgcn-amd-amdhsa-{ARCH}.s")
-    order = handoff_order_violations(hyb)
-    if order or not _kernels(open(hyb).read().splitlines(), "hybrid_kernel"):
-        detail = "\n".join(f"hybrid.s:{ln}: {what}" for ln, what in order[:20]) or "no hybrid kernel found"
-        raise RuntimeError(f"cross-workgroup hand-off out of order in the generated code:\n{detail}")
+    for unit, kernel in (("hybrid", "hybrid_kernel"), ("refill", "refill_kernel")):
+        asm = os.path.join(BUILD, f"{unit}-hip-amdgcn-amd-amdhsa-{ARCH}.s")
+        order = handoff_order_violations(asm, kernel)
+        if order or not _kernels(open(asm).read().splitlines(), kernel):
+            detail = "\n".join(f"{unit}.s:{ln}: {what}" for ln, what in order[:20]) or f"no {kernel} found"
+            raise RuntimeError(f"cross-workgroup hand-off out of order in the generated code:\n{detail}")
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -16,6 +16,7 @@ namespace {
 std::atomic<int> g_grid_override{0};
 std::atomic<int> g_resolve_path{0};            // 0 automatic, BKMOO_PATH_TWO_PASS, BKMOO_PATH_HYBRID
 std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the cooperative path's bounded waits
+std::atomic<int> g_refill_stream{4};           // vectors per row and thread the refill path always streams
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cu_count[kMaxDevices];
@@ -135,7 +136,7 @@ Carved carve(void *ws, const Layout &L) {
 // there.
 template <int (*Grid)(int, int, int)>
 int cached_grid(int K, int dt, int out_dt) {
-  static std::atomic<int> cache[kMaxDevices][kHybridMaxK - 1][2][2];  // K-2, dt, out_dt: 0 unknown, -1 none
+  static std::atomic<int> cache[kMaxDevices][kMaxK - 1][2][2];  // K-2, dt, out_dt: 0 unknown, -1 none
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
     const int g = Grid(K, dt, out_dt);
@@ -249,7 +250,8 @@ HybLayout hybrid_layout(int K, int dt, int method, int iters, int64_t N, int B, 
 int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters,
                   int64_t cap_slots) {
   const int mode = g_resolve_path.load();
-  if (mode == BKMOO_PATH_TWO_PASS || K > kHybridMaxK || !vec || is_exact(method)) return 0;
+  if (mode == BKMOO_PATH_TWO_PASS || mode == BKMOO_PATH_REFILL || K > kHybridMaxK || !vec || is_exact(method))
+    return 0;
   const int g = cached_grid<hybrid_grid>(K, dt, out_dt);
   if (g <= 0) return 0;
   const int gd = hybrid_data_workgroups(g);
@@ -262,6 +264,32 @@ int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
   const double base_mib = kHybridBaseMiB > kHybridBaseMiBPerRow * K ? kHybridBaseMiB : kHybridBaseMiBPerRow * K;
   const double min_bytes = (base_mib + kHybridMiBPerUs * solve_latency_us(method, K, iters)) * (1 << 20);
   return B >= kHybridMinBuckets && bucket_bytes >= min_bytes && held >= kHybridMinHeld ? g : 0;
+}
+
+// Workgroups for the single-buffer pipelined path, or 0 when it should not
+// be used.  Automatically only where the two-buffer kernel cannot run (K =
+// 9, 10) and each bucket carries enough data to hide its hand-off: the same
+// size rule as the two-buffer path, without its share-kept-on-chip floor.
+// Measured on MI355X, K=10 fp32 (1.72B elements), ms per call, two passes /
+// refill: 25 MiB per row MGDA FW-20 22.96 / 20.28, PCGrad 22.91 / 20.41,
+// CAGrad FW-20 22.97 / 20.56; 100 MiB 22.96 / 22.55 (MGDA and CAGrad);
+// 5 MiB CAGrad FW-20 23.16 / 60.3 (the hand-off exposed at every bucket).
+// Up to K = 8 the two-buffer kernel is as fast or faster where both run
+// (K=8 bf16 25 MiB CAGrad FW-20 36.4 / 38.9, MGDA 36.7 / 36.2; K=6 bf16
+// MGDA 3.42 / 3.75, CAGrad 3.57 / 4.48; K=4 mean 16.1 / 18.9).
+int choose_refill(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters) {
+  const int mode = g_resolve_path.load();
+  if (mode == BKMOO_PATH_TWO_PASS || mode == BKMOO_PATH_HYBRID || K > kRefillMaxK || !vec || is_exact(method))
+    return 0;
+  const int g = cached_grid<refill_grid>(K, dt, out_dt);
+  if (g <= 0) return 0;
+  if ((N / (g - kHybridSolvers) + 2 * 4096) * (int64_t)elem_bytes(dt) >= ((int64_t)1 << 31)) return 0;
+  if (mode == BKMOO_PATH_REFILL) return g;
+  if (K <= kHybridMaxK || B < kHybridMinBuckets) return 0;
+  const double bucket_bytes = (double)N / B * K * elem_bytes(dt);
+  const double base_mib = kHybridBaseMiB > kHybridBaseMiBPerRow * K ? kHybridBaseMiB : kHybridBaseMiBPerRow * K;
+  const double min_bytes = (base_mib + kHybridMiBPerUs * solve_latency_us(method, K, iters)) * (1 << 20);
+  return bucket_bytes >= min_bytes ? g : 0;
 }
 
 // bkmoo_resolve's argument checks (everything but the workspace); the
@@ -419,6 +447,16 @@ bkmoo_status resolve_impl(int32_t K, const void *const *grads, bkmoo_dtype dt, i
   const double c = hp ? hp->cagrad_c : 0.0;
   const int8_t *order = hp ? hp->pcgrad_order : nullptr;
 
+  const int rgrid = choose_refill(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters);
+  if (rgrid > 0) {
+    hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start, nullptr,
+                                   w.err, nullptr, 0, stream);
+    if (e != hipSuccess) return BKMOO_EHIP;
+    e = launch_refill(K, (int)dt, (int)out_dt, grads, bucket_offsets, B, shift, (int)method, iters, c, order,
+                      G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride, w.err, g_spin_limit.load(),
+                      rgrid, g_refill_stream.load(), stream);
+    return hip_status(e);
+  }
   const int hgrid =
       choose_hybrid(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters, L.cap_chunks);
   if (hgrid > 0) {
@@ -499,6 +537,29 @@ bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_
     *bytes = once + (uint64_t)K * s * (uint64_t)N;
     return BKMOO_OK;
   }
+  if (path == BKMOO_PATH_REFILL) {
+    if (K > 10) return BKMOO_EUNSUPPORTED;
+    const int g = refill_grid(K, (int)dt, (int)out_dt);
+    if (g <= 0) return BKMOO_EUNSUPPORTED;
+    const HybLayout lay{g - kHybridSolvers, 0, 0, 0};
+    const int64_t unit = hybrid_unit_elems((int)dt), held_max = refill_held_elems(K, (int)dt);
+    const int64_t smin = (int64_t)g_refill_stream.load() * unit;
+    uint64_t reread = 0;
+    for (int b = 0; b < B; ++b) {  // each segment re-reads what it did not keep
+      const int64_t n = offsets_host[b + 1] - offsets_host[b];
+      int64_t lo, hi, nseg, ns;
+      lay.segment(n, 0, unit, lo, hi, nseg);
+      for (int w = 0; w < nseg; ++w) {
+        lay.segment(n, w, unit, lo, hi, ns);
+        const int64_t len = hi - lo, slots = (len + unit - 1) / unit;
+        int64_t keep = slots * unit - smin;
+        keep = keep < 0 ? 0 : keep > held_max ? held_max : keep;
+        if (len > keep) reread += (uint64_t)(len - keep);
+      }
+    }
+    *bytes = once + (uint64_t)K * s * reread;
+    return BKMOO_OK;
+  }
   if (path != BKMOO_PATH_HYBRID) return BKMOO_EINVAL;
   if (K > kHybridMaxK) return BKMOO_EUNSUPPORTED;
   int dev = 0;
@@ -547,8 +608,10 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
   if (st != BKMOO_OK) return st;
   if (!valid_dtype(out_dt) || method < BKMOO_MGDA || method > BKMOO_CAGRAD_EXACT) return BKMOO_EINVAL;
   if (k_unsupported(K, method)) return BKMOO_EUNSUPPORTED;
-  if (choose_hybrid(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter,
-                    layout(K, N, B, dt).cap_chunks) > 0)
+  if (choose_refill(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter) > 0)
+    *path = BKMOO_PATH_REFILL;
+  else if (choose_hybrid(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter,
+                         layout(K, N, B, dt).cap_chunks) > 0)
     *path = BKMOO_PATH_HYBRID;
   else
     *path = BKMOO_PATH_TWO_PASS;
@@ -556,8 +619,15 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
 }
 
 bkmoo_status bkmoo_set_resolve_path(int32_t path) {
-  if (path != 0 && path != BKMOO_PATH_TWO_PASS && path != BKMOO_PATH_HYBRID) return BKMOO_EINVAL;
+  if (path != 0 && path != BKMOO_PATH_TWO_PASS && path != BKMOO_PATH_HYBRID && path != BKMOO_PATH_REFILL)
+    return BKMOO_EINVAL;
   g_resolve_path.store(path);
+  return BKMOO_OK;
+}
+
+bkmoo_status bkmoo_set_refill_stream(int32_t vectors) {
+  if (vectors < 0) return BKMOO_EINVAL;
+  g_refill_stream.store(vectors);
   return BKMOO_OK;
 }
 

@@ -391,28 +391,12 @@ struct Hybrid {
         double wt = 0.0, ax = 0.0;
         if (a.method == PCGRAD || sm.S.bad) {
           solver_run<WaveSync>(sm.S, K, a.method, a.iters, a.c, a.order, b, t, &wt, &ax);
+        } else if (a.method == MGDA) {
+          wt = ax = lane_solve_mgda<K>(sm.S.G, a.iters, t);
+        } else if (a.method == CAGRAD) {
+          lane_solve_cagrad<K>(sm.S.G, a.iters, a.c, t, &wt, &ax);
         } else {
-          double Gr[K][K], wr[K], xr[K];
-#pragma unroll
-          for (int i = 0; i < K; ++i)
-#pragma unroll
-            for (int j = 0; j < K; ++j) Gr[i][j] = sm.S.G[i * K + j];
-          if (a.method == MGDA) {
-            reg_solve_mgda<K>(Gr, a.iters, xr);
-#pragma unroll
-            for (int i = 0; i < K; ++i) wr[i] = xr[i];
-          } else if (a.method == CAGRAD) {
-            reg_solve_cagrad<K>(Gr, a.iters, a.c, wr, xr);
-          } else {
-#pragma unroll
-            for (int i = 0; i < K; ++i) wr[i] = xr[i] = 1.0 / (double)K;
-          }
-#pragma unroll
-          for (int i = 0; i < K; ++i)
-            if (t == i) {
-              wt = wr[i];
-              ax = xr[i];
-            }
+          wt = ax = 1.0 / (double)K;
         }
         // lane i < K holds task i's weight and variable; thread 0 gathers them
         // and publishes the weights, then the flag

@@ -11,6 +11,7 @@ constexpr int kMinK = 2;
 constexpr int kMaxK = 16;
 constexpr int kExactMaxK = 10;  // exact solvers: 2^K - 1 supports per bucket
 constexpr int kHybridMaxK = 8;  // the pipelined cooperative resolve (hybrid.hip)
+constexpr int kRefillMaxK = 10; // the single-buffer pipelined resolve (refill.hip)
 constexpr int kThreads = 256;          // streaming kernels: 4 wavefronts of 64
 constexpr int kWave = 64;
 
@@ -71,7 +72,8 @@ constexpr int kFlagCopies = 8;
 //   chunk_start         int64 [B + 1]     (prefix sum of chunks per bucket)
 //   gram                fp64  [B][K][K]   (used when the caller passes none)
 //   weights             fp32  [B][K]      (used when the caller passes none)
-//   partials            fp64  [cap][P]    cap = ceil(N / C) + B
+//   partials            fp64  [cap][P]    cap = ceil(N / C) + B (at least kCoopSlots slots of P
+//                                         rounded up to even)
 //   group_start         int64 [B + 1]     (prefix sum of finalize groups per bucket)
 //   groups              fp64  [gcap][P]   gcap = cap / kFinalizeGroup + B + 1
 //   sync                uint32 [1 + kFlagCopies][B][kSyncStride]  cooperative path: arrival
@@ -94,7 +96,10 @@ inline Layout layout(int K, int64_t N, int B, int dt) {
   L.chunk_start = o;    o = align256(o + sizeof(int64_t) * (size_t)(B + 1));
   L.gram = o;           o = align256(o + sizeof(double) * (size_t)B * K * K);
   L.weights = o;        o = align256(o + sizeof(float) * (size_t)B * K);
-  L.partials = o;       o = align256(o + sizeof(double) * (size_t)L.cap_chunks * pairs(K));
+  // (the single-buffer cooperative kernel pads each slot to an even count)
+  const int64_t part = L.cap_chunks * pairs(K) > kCoopSlots * (pairs(K) + (pairs(K) & 1))
+                           ? L.cap_chunks * pairs(K) : kCoopSlots * (pairs(K) + (pairs(K) & 1));
+  L.partials = o;       o = align256(o + sizeof(double) * (size_t)part);
   L.cap_groups = L.cap_chunks / kFinalizeGroup + B + 1;
   L.group_start = o;    o = align256(o + sizeof(int64_t) * (size_t)(B + 1));
   L.groups = o;         o = align256(o + sizeof(double) * (size_t)L.cap_groups * pairs(K));
@@ -219,6 +224,18 @@ hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, con
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
                          uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid,
                          const HybLayout &layout, hipStream_t s);
+
+// Single-buffer pipelined resolve (K <= 4, refill.hip): cooperative grid
+// (0 if it cannot run), elements of a segment it can keep on chip, launch.
+// Its data workgroups hold equal segments; `stream_min` vectors per row and
+// thread of each segment are always streamed.
+int refill_grid(int K, int dt, int out_dt);
+int64_t refill_held_elems(int K, int dt);
+hipError_t launch_refill(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
+                         int shift, int method, int iters, double c, const int8_t *order, double *gram,
+                         float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
+                         uint32_t *recs, uint32_t *err, uint32_t spin_limit, int grid, int stream_min,
+                         hipStream_t s);
 
 int device_cu_count();
 

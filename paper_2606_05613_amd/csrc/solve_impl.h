@@ -425,6 +425,225 @@ __device__ void reg_solve_cagrad(const double (&G)[K][K], int iters, double c, d
   for (int i = 0; i < K; ++i) wt[i] = degenerate ? invK : invK + (r / nrm) * w[i];
 }
 
+// ---- lane-parallel solvers for a compile-time K <= 16 ---------------------
+// The same algorithms as solve_mgda and solve_cagrad above (same start,
+// steps, tie rules, line searches and fixed iteration counts), run by one
+// whole wavefront with lane i < K holding task i's row of G, its entry of
+// G a and its variable, so a step costs O(K) instead of O(K^2) arithmetic
+// per lane.  Cross-lane steps use DPP within the first row of 16 lanes
+// (quad butterflies, then rotations by 4 and 8), and lane 0's result is
+// broadcast; sums are therefore added in a different (fixed) order than the
+// sequential loops above, so results agree with them to rounding, not
+// bitwise.  Used where one bucket's solve sits on a critical path.
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xf, 0xf, false);
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const long long u = __double_as_longlong(x);
+  const int lo = dpp_i32<CTRL>((int)u), hi = dpp_i32<CTRL>((int)(u >> 32));
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+// x of lane l (l uniform across the wavefront).
+__device__ __forceinline__ double lane_f64(double x, int l) {
+  const long long u = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_readlane((int)u, l), hi = __builtin_amdgcn_readlane((int)(u >> 32), l);
+  return __longlong_as_double((long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo));
+}
+// DPP controls: quad_perm xor 1, quad_perm xor 2, row rotations by 4 and 8.
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppRor4 = 0x124, kDppRor8 = 0x128;
+
+// Sum of x over lanes 0..K-1 (x must be 0 on lanes K..15), broadcast.
+template <int K>
+__device__ __forceinline__ double row_sum(double x) {
+  static_assert(K <= 16, "one row of lanes");
+  x += dpp_f64<kDppXor1>(x);
+  x += dpp_f64<kDppXor2>(x);
+  if constexpr (K > 4) {
+    x += dpp_f64<kDppRor4>(x);
+    x += dpp_f64<kDppRor8>(x);
+  }
+  return lane_f64(x, 0);
+}
+
+template <int CTRL>
+__device__ __forceinline__ void argmin_step(double &v, int &idx) {
+  const double ov = dpp_f64<CTRL>(v);
+  const int oi = dpp_i32<CTRL>(idx);
+  const bool take = ov < v || (ov == v && oi < idx);
+  v = take ? ov : v;
+  idx = take ? oi : idx;
+}
+// Lowest index among the least v over lanes 0..K-1 (v must be +inf and idx
+// above K on lanes K..15), broadcast.
+template <int K>
+__device__ __forceinline__ int row_argmin(double v, int idx) {
+  static_assert(K <= 16, "one row of lanes");
+  argmin_step<kDppXor1>(v, idx);
+  argmin_step<kDppXor2>(v, idx);
+  if constexpr (K > 4) {
+    argmin_step<kDppRor4>(v, idx);
+    argmin_step<kDppRor8>(v, idx);
+  }
+  return __builtin_amdgcn_readlane(idx, 0);
+}
+
+// First pair (i < j, lexicographic) of least two-point norm and its step:
+// lane l < K(K-1)/2 evaluates pair l, then a wavefront-wide lexicographic
+// (value, pair) minimum.  Every lane returns the same (bi, bj, bg).
+template <int K>
+__device__ __forceinline__ void lane_best_pair(const double *G, int lane, int &bi, int &bj, double &bg) {
+  constexpr int NP = K * (K - 1) / 2;
+  static_assert(NP <= kWave, "one pair per lane");
+  int pi = 0, rem = lane < NP ? lane : 0;
+  while (rem >= K - 1 - pi) {
+    rem -= K - 1 - pi;
+    ++pi;
+  }
+  const int pj = pi + 1 + rem;
+  const double aa = G[pi * K + pi], ab = G[pi * K + pj], bb = G[pj * K + pj];
+  const double g = pair_gamma(aa, ab, bb);
+  double val = lane < NP ? pair_value(g, aa, ab, bb) : __builtin_inf();
+  int idx = lane < NP ? lane : kWave;
+#pragma unroll
+  for (int off = kWave / 2; off >= 1; off >>= 1) {
+    const double ov = __shfl_xor(val, off, kWave);
+    const int oi = __shfl_xor(idx, off, kWave);
+    const bool take = ov < val || (ov == val && oi < idx);
+    val = take ? ov : val;
+    idx = take ? oi : idx;
+  }
+  const int best = __builtin_amdgcn_readfirstlane(idx);
+  bi = __builtin_amdgcn_readlane(pi, best);
+  bj = __builtin_amdgcn_readlane(pj, best);
+  bg = lane_f64(g, best);
+}
+
+// MGDA (as solve_mgda).  G: K x K row-major, readable by every lane (LDS).
+// Lane i < K returns task i's simplex weight.
+template <int K>
+__device__ double lane_solve_mgda(const double *G, int iters, int lane) {
+  const bool task = lane < K;
+  const int me = task ? lane : 0;
+  double gi[K], a[K];
+  double gd = 0.0;
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    gi[j] = task ? G[me * K + j] : 0.0;
+    gd = j == me ? gi[j] : gd;
+  }
+  int bi, bj;
+  double bg;
+  lane_best_pair<K>(G, lane, bi, bj, bg);
+#pragma unroll
+  for (int j = 0; j < K; ++j) a[j] = j == bi ? bg : j == bj ? 1.0 - bg : 0.0;
+  double own = task ? (me == bi ? bg : me == bj ? 1.0 - bg : 0.0) : 0.0;
+  for (int it = 0; it < iters; ++it) {
+    double v = 0.0;
+#pragma unroll
+    for (int j = 0; j < K; ++j) v += gi[j] * a[j];
+    const int t = row_argmin<K>(task ? v : __builtin_inf(), task ? lane : kWave);
+    const double aa = row_sum<K>(task ? own * v : 0.0);
+    const double g = pair_gamma(aa, lane_f64(v, t), lane_f64(gd, t));
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      double na = g * a[j];
+      if (j == t) na += 1.0 - g;
+      a[j] = na;
+    }
+    double no = g * own;
+    if (task && lane == t) no += 1.0 - g;
+    own = no;
+  }
+  return own;
+}
+
+// CAGrad (as solve_cagrad and cagrad_primal).  Lane i < K returns task i's
+// combine weight in *wt and dual variable in *w_out.
+template <int K>
+__device__ void lane_solve_cagrad(const double *G, int iters, double c, int lane, double *wt, double *w_out) {
+  const bool task = lane < K;
+  const int me = task ? lane : 0;
+  const double invK = 1.0 / (double)K;
+  double gi[K], w[K];
+  double gd = 0.0, rs = 0.0;
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    gi[j] = task ? G[me * K + j] : 0.0;
+    gd = j == me ? gi[j] : gd;
+    rs += gi[j];
+    w[j] = invK;
+  }
+  const double bo = rs / (double)K;  // b_i = (G 1)_i / K
+  double g0sq = row_sum<K>(task ? rs : 0.0) / (double)(K * K);
+  g0sq = g0sq > 0.0 ? g0sq : 0.0;
+  const double r = c * sqrt(g0sq);
+  double own = task ? invK : 0.0;
+  for (int it = 0; it < iters; ++it) {
+    double v = 0.0;
+#pragma unroll
+    for (int j = 0; j < K; ++j) v += gi[j] * w[j];
+    const double cq = row_sum<K>(task ? own * v : 0.0);
+    const double bw = row_sum<K>(task ? bo * own : 0.0);
+    const double nrm = sqrt(cq > 0.0 ? cq : 0.0);
+    const double grad = bo + (nrm > 1e-300 ? r * v / nrm : 0.0);
+    const int s = row_argmin<K>(task ? grad : __builtin_inf(), task ? lane : kWave);
+    const double vs = lane_f64(v, s);
+    const double beta1 = lane_f64(bo, s) - bw;
+    const double A = lane_f64(gd, s) - 2.0 * vs + cq;
+    const double Bq = vs - cq;
+    double g1 = -1.0, g2 = -1.0;
+    const double D = r * r * A - beta1 * beta1;
+    if (A > 0.0 && D > 0.0) {
+      const double disc = (A * cq - Bq * Bq) / D;
+      if (disc >= 0.0) {
+        const double root = fabs(beta1) * sqrt(disc);
+        g1 = (-Bq - root) / A;
+        g2 = (-Bq + root) / A;
+      }
+    }
+    // candidates in ascending order on lanes 0..3: 0, the interior
+    // stationary points (g1 <= g2 since A > 0), 1; the first of least F wins
+    const int q4 = lane & 3;
+    const double gc = q4 == 0 ? 0.0 : q4 == 1 ? g1 : q4 == 2 ? g2 : 1.0;
+    const bool valid = lane < 4 && (q4 == 0 || q4 == 3 || (gc > 0.0 && gc < 1.0));
+    double qq = A * gc * gc + 2.0 * Bq * gc + cq;
+    qq = qq > 0.0 ? qq : 0.0;
+    const double f = valid ? bw + beta1 * gc + r * sqrt(qq) : __builtin_inf();
+    double fv = f;
+    int fi = valid ? q4 : kWave;
+    argmin_step<kDppXor1>(fv, fi);
+    argmin_step<kDppXor2>(fv, fi);
+    const double gamma = lane_f64(gc, __builtin_amdgcn_readlane(fi, 0));
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      double nw = (1.0 - gamma) * w[j];
+      if (j == s) nw += gamma;
+      w[j] = nw;
+    }
+    double no = (1.0 - gamma) * own;
+    if (task && lane == s) no += gamma;
+    own = no;
+  }
+  double v = 0.0;
+#pragma unroll
+  for (int j = 0; j < K; ++j) v += gi[j] * w[j];
+  const double q = row_sum<K>(task ? own * v : 0.0);
+  double dmax = 0.0;
+#pragma unroll
+  for (int l = 0; l < K; ++l) {
+    const double x = lane_f64(gd, l);
+    dmax = x > dmax ? x : dmax;
+  }
+  const double nrm = sqrt(q > 0.0 ? q : 0.0);
+  const double scale = sqrt(dmax);
+  const bool degenerate = r == 0.0 || nrm <= 1e-12 * scale || nrm == 0.0;
+  *wt = degenerate ? invK : invK + (r / nrm) * own;
+  *w_out = own;
+}
+
 // Load one bucket's Gram matrix (fp64, row-major K x K) into S and flag a
 // non-finite entry.  Returns through S.bad.
 template <typename Sync>

@@ -99,8 +99,9 @@ def test_handoff_order_flags_missing_points(tmp_path):
     assert len(_order(tmp_path, no_loop)) == 1
 
 
-def test_built_hybrid_kernel_hands_off_in_order():
-    asm = os.path.join(BUILD, "hybrid-hip-amdgcn-amd-amdhsa-gfx950.s")
+@pytest.mark.parametrize("unit", ["hybrid", "refill"])
+def test_built_cooperative_kernels_hand_off_in_order(unit):
+    asm = os.path.join(BUILD, f"{unit}-hip-amdgcn-amd-amdhsa-gfx950.s")
     if not os.path.exists(asm):
         pytest.skip("library not built")
-    assert handoff_order_violations(asm) == []
+    assert handoff_order_violations(asm, f"{unit}_kernel") == []

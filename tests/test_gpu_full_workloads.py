@@ -201,6 +201,12 @@ def test_full_qwen_k10_bucket_sweep(gpu_lib, mib):
     base = WORKLOADS[f"qwen-1.7b-k10-{mib}mib-mgda-f32"]
     grads = fill_grads(base, device="cuda")
     offs = torch.from_numpy(base.offsets()).cuda()
+    gpu_lib.set_resolve_path(0)
+    # 25 and 100 MiB buckets take the single-buffer cooperative kernel, the
+    # smaller ones the two passes (their hand-off per bucket would show)
+    want = gpu_lib.PATH_REFILL if mib >= 25 else gpu_lib.PATH_TWO_PASS
+    for m in ("mgda", "pcgrad", "cagrad"):
+        assert gpu_lib.resolve_path(grads, base.B + 1, m, 20 if m != "pcgrad" else 0) == want, (mib, m)
     try:
         grams = {}
         for m in ("mgda", "pcgrad", "cagrad"):

@@ -76,13 +76,13 @@ TILE_BUCKET = 3 << 19   # elements per bucket: whole 2- and 3-element repeats, a
 TILE_B = 12
 
 
-@pytest.mark.parametrize("path", ["two-pass", "hybrid"])
+@pytest.mark.parametrize("path", ["two-pass", "hybrid", "refill"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("case", CASES, ids=[c["name"] for c in CASES])
 def test_golden_tiled(gpu_lib, case, dtype, path):
     lib = gpu_lib
     dev = torch.device("cuda", 0)
-    p = {"two-pass": lib.PATH_TWO_PASS, "hybrid": lib.PATH_HYBRID}[path]
+    p = {"two-pass": lib.PATH_TWO_PASS, "hybrid": lib.PATH_HYBRID, "refill": lib.PATH_REFILL}[path]
     m = _method(case)
     g = torch.tensor(case["g"], dtype=torch.float64, device=dev)
     K, dim = g.shape

@@ -20,11 +20,13 @@ BASE = WORKLOADS["llama3-8b-k4-mgda-bf16"]
 LENS = [70_001, 1, 0, 33_333, 131_072, 7, 65_539, 40_047]
 
 
-@pytest.fixture
-def coop(gpu_lib):
-    """The library with the cooperative (hybrid) path forced, and that path."""
-    gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
-    yield gpu_lib, gpu_lib.PATH_HYBRID
+@pytest.fixture(params=["PATH_HYBRID", "PATH_REFILL"])
+def coop(gpu_lib, request):
+    """The library with a cooperative path forced (the two-buffer hybrid or
+    the single-buffer refill kernel), and that path."""
+    path = getattr(gpu_lib, request.param)
+    gpu_lib.set_resolve_path(path)
+    yield gpu_lib, path
     gpu_lib.set_resolve_path(0)
 
 
@@ -49,17 +51,21 @@ def test_coop_parity(coop, method, dtype, K):
 
 @pytest.mark.parametrize("method", ["mgda", "pcgrad", "cagrad", "mean"])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("K", [5, 6, 7, 8])
-def test_hybrid_parity_more_tasks(gpu_lib, method, dtype, K):
-    """The pipelined kernel for K = 5..8 (one or two kept register vectors,
-    one LDS vector, one or two streamed per step)."""
-    gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
+@pytest.mark.parametrize("K,path_name", [(K, p) for K in (5, 6, 7, 8) for p in ("PATH_HYBRID", "PATH_REFILL")]
+                         + [(K, "PATH_REFILL") for K in (9, 10)])
+def test_coop_parity_more_tasks(gpu_lib, method, dtype, K, path_name):
+    """The cooperative kernels for K = 5..10 (the two-buffer kernel up to
+    K = 8: one or two kept register vectors, one LDS vector, one or two
+    streamed per step; the single-buffer kernel up to K = 10)."""
+    path = getattr(gpu_lib, path_name)
+    gpu_lib.set_resolve_path(path)
     try:
         wl = small_workload(BASE, sum(LENS), bucket_lens=LENS, K=K, dtype=dtype, method=method,
                             seed=9100 + 10 * K + (dtype == "bf16"))
         grads, _, _ = to_device_inputs(wl)
-        assert gpu_lib.resolve_path(grads, wl.B + 1, method) == gpu_lib.PATH_HYBRID
-        print(f"case hybrid {wl.name} K={K} {dtype} {method}", full_parity(gpu_lib, wl, grads=grads), flush=True)
+        assert gpu_lib.resolve_path(grads, wl.B + 1, method) == path
+        print(f"case {path_name} {wl.name} K={K} {dtype} {method}", full_parity(gpu_lib, wl, grads=grads),
+              flush=True)
     finally:
         gpu_lib.set_resolve_path(0)
 
@@ -170,7 +176,7 @@ def test_coop_bucket_larger_than_chip(coop):
     print(full_parity(lib, wl, grads=grads), flush=True)
 
 
-@pytest.mark.parametrize("path_name", ["PATH_HYBRID"])
+@pytest.mark.parametrize("path_name", ["PATH_HYBRID", "PATH_REFILL"])
 def test_coop_deterministic_and_close_to_two_pass(gpu_lib, path_name):
     wl = small_workload(BASE, sum(LENS), bucket_lens=LENS, K=4, dtype="bf16", method="cagrad", seed=31)
     grads, offs, order = to_device_inputs(wl)

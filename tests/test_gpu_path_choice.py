@@ -77,13 +77,21 @@ def test_automatic_path_more_tasks(gpu_lib, K, B, method, iters, want):
     assert got == want, f"K={K} B={B} {method}-{iters}: {got}"
 
 
-def test_more_than_eight_tasks_run_two_passes(gpu_lib):
+def test_more_than_eight_tasks(gpu_lib):
+    """Nine tasks in 8 buckets of 16 MiB per row: beyond the two-buffer
+    kernel, so the single-buffer one takes them (forcing the two-buffer one
+    falls back to the two passes); eleven tasks only run the two passes,
+    whatever is forced."""
     g = torch.empty((9, 1 << 26), dtype=torch.bfloat16, device="cuda")
+    g11 = torch.empty((11, 1 << 24), dtype=torch.bfloat16, device="cuda")
     gpu_lib.set_resolve_path(0)
-    assert gpu_lib.resolve_path(g, 9, "mean", 0) == gpu_lib.PATH_TWO_PASS
-    gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
+    assert gpu_lib.resolve_path(g, 9, "mean", 0) == gpu_lib.PATH_REFILL
+    assert gpu_lib.resolve_path(g11, 9, "mean", 0) == gpu_lib.PATH_TWO_PASS
     try:
+        gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
         assert gpu_lib.resolve_path(g, 9, "mean", 0) == gpu_lib.PATH_TWO_PASS
+        gpu_lib.set_resolve_path(gpu_lib.PATH_REFILL)
+        assert gpu_lib.resolve_path(g11, 9, "mean", 0) == gpu_lib.PATH_TWO_PASS
     finally:
         gpu_lib.set_resolve_path(0)
 
@@ -107,14 +115,17 @@ def test_misaligned_rows_take_the_two_passes(gpu_lib):
 
 def test_forced_hybrid_and_unknown_paths(gpu_lib, rows_4x2g):
     """Forced, the hybrid path runs wherever it can (aligned rows, K <= 8,
-    iterative or not, any bucket count); a path value other than 0, 1 and 3
-    is rejected."""
+    iterative or not, any bucket count), and so does the refill path (K <= 10);
+    a path value other than 0, 1, 3 and 4 is rejected."""
     gpu_lib.set_resolve_path(gpu_lib.PATH_HYBRID)
     try:
         for B in (4, 48, 613):
             assert gpu_lib.resolve_path(rows_4x2g, B + 1, "mgda", 20) == gpu_lib.PATH_HYBRID
+        gpu_lib.set_resolve_path(gpu_lib.PATH_REFILL)
+        for B in (4, 48, 613):
+            assert gpu_lib.resolve_path(rows_4x2g, B + 1, "mgda", 20) == gpu_lib.PATH_REFILL
     finally:
         gpu_lib.set_resolve_path(0)
-    for bad in (-1, 2, 4):
+    for bad in (-1, 2, 5):
         with pytest.raises(gpu_lib.BkmooError):
             gpu_lib.set_resolve_path(bad)

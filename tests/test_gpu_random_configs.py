@@ -36,7 +36,8 @@ def _draw(case, cooperative):
     if sum(lens) == 0:
         lens[-1] = 16
     out_dt = None if rng.random() < 0.7 else (torch.float32 if dt == "bf16" else torch.bfloat16)
-    path = str(rng.choice(["PATH_HYBRID"] if cooperative else ["auto", "PATH_TWO_PASS", "PATH_HYBRID"]))
+    path = str(rng.choice(["PATH_HYBRID", "PATH_REFILL"] if cooperative
+                          else ["auto", "PATH_TWO_PASS", "PATH_HYBRID", "PATH_REFILL"]))
     wl = small_workload(BASES[dt], sum(lens), bucket_lens=lens, K=K, dtype=dt, method=method, max_iter=iters,
                         cagrad_c=c, seed=7_000 + 100 * cooperative + case)
     return wl, out_dt, path
