@@ -68,8 +68,8 @@ KERNEL_SOURCES = {
     "combine": ["combine.hip", "combine_impl.h", "stream_common.h", "internal.h"],
     "hybrid": ["hybrid.hip", "coop_common.h", "combine_impl.h", "solve_impl.h", "stream_common.h",
                "internal.h"],
-    "refill": ["refill.hip", "coop_common.h", "combine_impl.h", "solve_impl.h", "stream_common.h",
-               "internal.h"],
+    "refill": ["refill.hip", "refill.h", "coop_common.h", "combine_impl.h", "solve_impl.h",
+               "stream_common.h", "internal.h"],
 }
 
 

@@ -104,7 +104,7 @@ typedef enum {
   BKMOO_PATH_TWO_PASS = 1, /* Gram pass, solve, combine pass: reads the gradients twice */
   BKMOO_PATH_HYBRID = 3,   /* one cooperative kernel, part of each bucket held on chip, the next
                               bucket's Gram overlapping this one's solve */
-  BKMOO_PATH_REFILL = 4    /* one cooperative kernel (K <= 4), most of each bucket held on chip in
+  BKMOO_PATH_REFILL = 4    /* one cooperative kernel (K <= 10), part of each bucket held on chip in
                               one buffer refilled with the next bucket as it is combined */
 } bkmoo_path;
 
@@ -234,12 +234,20 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  *             expires the call still completes, sets BKMOO_DEVERR_TIMEOUT in
  *             the workspace error word, and the buckets concerned get NaN
  *             weights and a NaN update.
- * Automatic choice: the hybrid path for at least 8 buckets of which at
- * least 10% stays on chip, averaging (all K rows) at least max(24, 6 K)
- * MiB plus 4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA
- * iteration, 0.22 K us per CAGrad iteration, 0.1 K^2 us for PCGrad, 0 for
- * the mean), so that each bucket's hand-off is amortised; else the two
- * passes.  Exact solvers never take the cooperative path.
+ *   refill    (K <= 10, aligned as for hybrid) one cooperative kernel that
+ *             keeps up to twice the hybrid's share of each bucket on chip
+ *             in a single buffer: the part of bucket b+1 it does not keep
+ *             is read while bucket b is solved, then each kept vector of
+ *             bucket b is combined and replaced by bucket b+1's.  Rounding,
+ *             determinism and bounded waits as for hybrid.
+ * Automatic choice: for K <= 8 the hybrid path for at least 8 buckets of
+ * which at least 10% stays on chip, averaging (all K rows) at least
+ * max(24, 6 K) MiB plus 4 MiB per microsecond of estimated solve latency
+ * (0.07 K us per MGDA iteration, 0.22 K us per CAGrad iteration, 0.1 K^2 us
+ * for PCGrad, 0 for the mean), so that each bucket's hand-off is amortised;
+ * for K = 9, 10 the refill path under the same size rule without the
+ * on-chip share; else the two passes.  Exact solvers never take a
+ * cooperative path.
  * bkmoo_resolve_path reports the choice; bkmoo_set_resolve_path forces one.
  */
 bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,
@@ -352,7 +360,8 @@ bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *c
  *   BKMOO_PATH_TWO_PASS  2*K*s*N + s_out*N
  *   BKMOO_PATH_HYBRID    K*s*N + s_out*N, plus K*s per element a data
  *                        workgroup did not keep on chip (read twice)
- * with s, s_out the input and output element sizes.  The small per-bucket
+ * with s, s_out the input and output element sizes; BKMOO_PATH_REFILL as
+ *                        BKMOO_PATH_HYBRID with its own (larger) kept share.  The small per-bucket
  * terms (offsets, Gram matrices, weights, partial sums) are left out.  The
  * hybrid path depends on the current device's CU count, and its segments
  * also on the method and iteration count (`method`,
@@ -360,7 +369,8 @@ bkmoo_status bkmoo_conflicts(int32_t K, int32_t B, const double *gram, double *c
  * workgroup of each CU takes a longer segment.  BKMOO_EINVAL
  * for bad sizes or pointers, invalid offsets, method or iteration count, or
  * an unknown path;
- * BKMOO_EUNSUPPORTED for the hybrid path with K > 8; BKMOO_EHIP when the
+ * BKMOO_EUNSUPPORTED for the hybrid path with K > 8 or the refill path with
+ * K > 10; BKMOO_EHIP when the
  * current device cannot be queried.
  */
 bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_t *offsets_host,
@@ -385,8 +395,8 @@ bkmoo_status bkmoo_set_grid_override(int32_t workgroups);
 
 /*
  * bkmoo_resolve_path — the implementation bkmoo_resolve would use for these
- * arguments on the current device (*path, host): BKMOO_PATH_TWO_PASS or
- * BKMOO_PATH_HYBRID.  `aligned` says whether every row and the output
+ * arguments on the current device (*path, host): BKMOO_PATH_TWO_PASS,
+ * BKMOO_PATH_HYBRID or BKMOO_PATH_REFILL.  `aligned` says whether every row and the output
  * start at the same 16-byte phase.
  */
 bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt, bkmoo_dtype out_dt,
@@ -395,29 +405,21 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
 
 /*
  * bkmoo_set_resolve_path — force bkmoo_resolve's implementation
- * (0: automatic, BKMOO_PATH_TWO_PASS, or BKMOO_PATH_HYBRID when eligible:
- * K <= 8, aligned rows, not an exact method).  Process-wide; for tests and
- * tuning.  BKMOO_EINVAL for any other value.
+ * (0: automatic, BKMOO_PATH_TWO_PASS, or BKMOO_PATH_HYBRID or
+ * BKMOO_PATH_REFILL when eligible: K <= 8 or K <= 10, aligned rows, not an
+ * exact method; an ineligible call runs the two passes).  Process-wide; for
+ * tests and tuning.  BKMOO_EINVAL for any other value.
  */
 bkmoo_status bkmoo_set_resolve_path(int32_t path);
 
 /*
- * bkmoo_set_wait_limit — polls of the hybrid path's bounded waits (for
+ * bkmoo_set_wait_limit — polls of the cooperative paths' bounded waits (for
  * a bucket's arrivals or weights) before a workgroup gives up and sets
  * BKMOO_DEVERR_TIMEOUT
  * (default 4194304, about a second or more).  Process-wide; lets tests force
  * the timeout path from the host.  0 is rejected.
  */
 bkmoo_status bkmoo_set_wait_limit(uint32_t polls);
-
-/*
- * bkmoo_set_refill_stream — vectors of 16 bytes per task row and thread
- * that each data workgroup of the refill path always streams instead of
- * keeping on chip (default 4); the streamed part of two buckets is the
- * window that hides each bucket's hand-off.  Process-wide; for tuning.
- * Negative values are rejected.
- */
-bkmoo_status bkmoo_set_refill_stream(int32_t vectors);
 
 /* Human-readable name of a status code (static string). */
 const char *bkmoo_status_string(bkmoo_status st);

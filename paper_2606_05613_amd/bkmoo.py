@@ -65,7 +65,6 @@ def _load():
                                ctypes.POINTER(i32)],
         "bkmoo_set_resolve_path": [i32],
         "bkmoo_set_wait_limit": [u32],
-        "bkmoo_set_refill_stream": [i32],
         "bkmoo_status_string": [ctypes.c_int],
     }
     for name, args in sig.items():
@@ -81,7 +80,7 @@ EXPORTS = ("bkmoo_workspace_size", "bkmoo_gram", "bkmoo_solve", "bkmoo_combine",
            "bkmoo_resolve_noalloc",
            "bkmoo_conflicts", "bkmoo_slice_offsets", "bkmoo_gram_reduce", "bkmoo_resolve_traffic",
            "bkmoo_read_device_error", "bkmoo_set_grid_override", "bkmoo_resolve_path",
-           "bkmoo_set_resolve_path", "bkmoo_set_wait_limit", "bkmoo_set_refill_stream", "bkmoo_status_string")
+           "bkmoo_set_resolve_path", "bkmoo_set_wait_limit", "bkmoo_status_string")
 
 
 def status_string(st: int) -> str:
@@ -377,7 +376,7 @@ def set_grid_override(workgroups: int):
 
 def resolve_path(grads: Grads, bucket_offsets_len: int, method: str = "mgda", max_iter: int = 20,
                  out_dtype=None) -> int:
-    """PATH_TWO_PASS or PATH_HYBRID: what resolve() would run for these
+    """PATH_TWO_PASS, PATH_HYBRID or PATH_REFILL: what resolve() would run for these
     grads and method (output assumed aligned like the rows)."""
     arr, dt, K, N, dev, rows = _rows(grads)
     B = bucket_offsets_len - 1
@@ -406,14 +405,9 @@ def resolve_traffic(K: int, bucket_offsets, dtype, path: int, out_dtype=None, me
 
 
 def set_resolve_path(path: int):
-    """0 automatic, PATH_TWO_PASS or PATH_HYBRID (process-wide)."""
+    """0 automatic, PATH_TWO_PASS, PATH_HYBRID or PATH_REFILL (process-wide)."""
     _check(_lib.bkmoo_set_resolve_path(int(path)), "bkmoo_set_resolve_path")
 
 
 def set_wait_limit(polls: int):
     _check(_lib.bkmoo_set_wait_limit(int(polls)), "bkmoo_set_wait_limit")
-
-
-def set_refill_stream(vectors: int):
-    """Vectors per row and thread the refill path always streams (process-wide)."""
-    _check(_lib.bkmoo_set_refill_stream(int(vectors)), "bkmoo_set_refill_stream")

@@ -8,6 +8,7 @@
 
 #include "bkmoo.h"
 #include "internal.h"
+#include "refill.h"
 
 namespace bkmoo {
 
@@ -16,7 +17,6 @@ namespace {
 std::atomic<int> g_grid_override{0};
 std::atomic<int> g_resolve_path{0};            // 0 automatic, BKMOO_PATH_TWO_PASS, BKMOO_PATH_HYBRID
 std::atomic<uint32_t> g_spin_limit{1u << 22};  // polls of the cooperative path's bounded waits
-std::atomic<int> g_refill_stream{4};           // vectors per row and thread the refill path always streams
 
 constexpr int kMaxDevices = 64;
 std::atomic<int> g_cu_count[kMaxDevices];
@@ -266,30 +266,78 @@ int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
   return B >= kHybridMinBuckets && bucket_bytes >= min_bytes && held >= kHybridMinHeld ? g : 0;
 }
 
-// Workgroups for the single-buffer pipelined path, or 0 when it should not
-// be used.  Automatically only where the two-buffer kernel cannot run (K =
-// 9, 10) and each bucket carries enough data to hide its hand-off: the same
-// size rule as the two-buffer path, without its share-kept-on-chip floor.
-// Measured on MI355X, K=10 fp32 (1.72B elements), ms per call, two passes /
-// refill: 25 MiB per row MGDA FW-20 22.96 / 20.28, PCGrad 22.91 / 20.41,
-// CAGrad FW-20 22.97 / 20.56; 100 MiB 22.96 / 22.55 (MGDA and CAGrad);
-// 5 MiB CAGrad FW-20 23.16 / 60.3 (the hand-off exposed at every bucket).
-// Up to K = 8 the two-buffer kernel is as fast or faster where both run
-// (K=8 bf16 25 MiB CAGrad FW-20 36.4 / 38.9, MGDA 36.7 / 36.2; K=6 bf16
-// MGDA 3.42 / 3.75, CAGrad 3.57 / 4.48; K=4 mean 16.1 / 18.9).
+// Groups of data workgroups for the single-buffer path: group g takes
+// buckets g, g + groups, ..., so a bucket's hand-off hides behind a round of
+// `groups` buckets of streaming instead of one.  A round of about
+// kRefillRoundMiB (all rows) is long enough to hide it and short enough
+// for the streamed part to be re-read from the 256 MB Infinity Cache;
+// beyond ~kRefillMaxRoundMiB the re-reads miss.  Measured on MI355X (ms per
+// call, two passes / refill at the groups the rule picks; best nearby
+// count in brackets): K=10 fp32 1.72B elements, 1 MiB per row CAGrad FW-20
+// 25.3 / 18.6 (G=18; 14: 18.6, 22: 22.5, 8: 33.6), MGDA 25.1 / 18.5,
+// PCGrad 25.1 / 18.3; 5 MiB CAGrad 23.2 / 18.1 (G=4; 3: 19.9, 5: 20.1),
+// MGDA 22.7 / 18.2, PCGrad 22.7 / 17.9; 25 MiB CAGrad 25.1 / 22.3 (G=1;
+// 2: 25.7); 100 MiB (G=1, a 1 GB round) 25.2 / 26.2.  K=4 bf16 2.1B
+// elements, 1 MiB MGDA 6.6 / 4.5 (G=32), CAGrad 6.7 / 5.1; 5 MiB MGDA
+// 6.6 / 4.5 (G=9; 6: 4.3), CAGrad 6.6 / 4.7.  K=8 bf16 1.07B elements,
+// 1 MiB MGDA 6.3 / 4.9 (G=24), CAGrad 6.3 / 5.0; 5 MiB MGDA 6.3 / 4.9
+// (G=4), CAGrad 6.3 / 5.3.
+constexpr double kRefillRoundMiB = 180.0;
+constexpr double kRefillMaxRoundMiB = 300.0;
+// A round must also cover the hand-off: at least this much, plus this much
+// per microsecond of estimated solve latency.
+constexpr double kRefillMinRoundMiB = 64.0, kRefillMiBPerUs = 2.0;
+// Where both cooperative kernels can run (K <= 8, large buckets) the
+// two-buffer one is as fast or faster except for long solves at K <= 4
+// (25 MiB per row, bf16, ms, two-buffer / refill: K=4 CAGrad FW-20 18.96 /
+// 16.85 (G=2), MGDA FW-20 17.31 / 17.15, PCGrad 16.06 / 17.17; K=8 CAGrad
+// FW-20 36.4 / 39.4 (G=1), 41.0 (G=2); K=6 MGDA 3.42 / 3.75).
+constexpr double kRefillOverHybridUs = 10.0;
+
+int refill_groups(int K, int dt, int64_t N, int B) {
+  const double bucket_mib = (double)N / B * K * elem_bytes(dt) / (1 << 20);
+  int g = (int)(kRefillRoundMiB / (bucket_mib > 1e-9 ? bucket_mib : 1e-9) + 0.5);
+  g = g < 1 ? 1 : g > kRefMaxGroups ? kRefMaxGroups : g;
+  return g < B ? g : (B > 0 ? B : 1);
+}
+
+// Workgroups for the single-buffer pipelined path if it can run and, unless
+// forced, its own size rule holds (the choice against the two-buffer path
+// is made in pick_path); else 0.
 int choose_refill(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters) {
   const int mode = g_resolve_path.load();
   if (mode == BKMOO_PATH_TWO_PASS || mode == BKMOO_PATH_HYBRID || K > kRefillMaxK || !vec || is_exact(method))
     return 0;
   const int g = cached_grid<refill_grid>(K, dt, out_dt);
   if (g <= 0) return 0;
-  if ((N / (g - kHybridSolvers) + 2 * 4096) * (int64_t)elem_bytes(dt) >= ((int64_t)1 << 31)) return 0;
+  const int groups = refill_groups(K, dt, N, B);
+  // a segment (at most N over one group's data workgroups) within one
+  // 32-bit buffer range
+  if ((N / ((g - refill_solvers(groups)) / groups) + 2 * 4096) * (int64_t)elem_bytes(dt) >= ((int64_t)1 << 31))
+    return 0;
   if (mode == BKMOO_PATH_REFILL) return g;
-  if (K <= kHybridMaxK || B < kHybridMinBuckets) return 0;
-  const double bucket_bytes = (double)N / B * K * elem_bytes(dt);
-  const double base_mib = kHybridBaseMiB > kHybridBaseMiBPerRow * K ? kHybridBaseMiB : kHybridBaseMiBPerRow * K;
-  const double min_bytes = (base_mib + kHybridMiBPerUs * solve_latency_us(method, K, iters)) * (1 << 20);
-  return bucket_bytes >= min_bytes ? g : 0;
+  if (B < kHybridMinBuckets) return 0;
+  const double round_mib = (double)N / B * K * elem_bytes(dt) / (1 << 20) * groups;
+  const double min_mib = kRefillMinRoundMiB + kRefillMiBPerUs * solve_latency_us(method, K, iters);
+  return round_mib >= min_mib && round_mib <= kRefillMaxRoundMiB ? g : 0;
+}
+
+// The path bkmoo_resolve takes and its grid (0 for the two passes).
+int pick_path(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method, int iters, int64_t cap_slots,
+              int *grid) {
+  const int rg = choose_refill(K, dt, out_dt, N, B, vec, method, iters);
+  const int hg = choose_hybrid(K, dt, out_dt, N, B, vec, method, iters, cap_slots);
+  const bool prefer_refill = K <= 4 && solve_latency_us(method, K, iters) >= kRefillOverHybridUs;
+  if (rg > 0 && (hg <= 0 || prefer_refill || g_resolve_path.load() == BKMOO_PATH_REFILL)) {
+    *grid = rg;
+    return BKMOO_PATH_REFILL;
+  }
+  if (hg > 0) {
+    *grid = hg;
+    return BKMOO_PATH_HYBRID;
+  }
+  *grid = 0;
+  return BKMOO_PATH_TWO_PASS;
 }
 
 // bkmoo_resolve's argument checks (everything but the workspace); the
@@ -447,19 +495,20 @@ bkmoo_status resolve_impl(int32_t K, const void *const *grads, bkmoo_dtype dt, i
   const double c = hp ? hp->cagrad_c : 0.0;
   const int8_t *order = hp ? hp->pcgrad_order : nullptr;
 
-  const int rgrid = choose_refill(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters);
-  if (rgrid > 0) {
+  int pgrid = 0;
+  const int path = pick_path(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters, L.cap_chunks,
+                             &pgrid);
+  if (path == BKMOO_PATH_REFILL) {
     hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start, nullptr,
                                    w.err, nullptr, 0, stream);
     if (e != hipSuccess) return BKMOO_EHIP;
     e = launch_refill(K, (int)dt, (int)out_dt, grads, bucket_offsets, B, shift, (int)method, iters, c, order,
                       G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride, w.err, g_spin_limit.load(),
-                      rgrid, g_refill_stream.load(), stream);
+                      pgrid, refill_groups(K, (int)dt, N, B), stream);
     return hip_status(e);
   }
-  const int hgrid =
-      choose_hybrid(K, (int)dt, (int)out_dt, N, B, vec_in && vec_out, (int)method, iters, L.cap_chunks);
-  if (hgrid > 0) {
+  if (path == BKMOO_PATH_HYBRID) {
+    const int hgrid = pgrid;
     hipError_t e = launch_schedule(bucket_offsets, B, N, gram_chunk_elems(K, dt), w.chunk_start,
                                    nullptr, w.err, w.sync, (1 + kFlagCopies) * (int64_t)B * kSyncStride, stream);
     if (e != hipSuccess) return BKMOO_EHIP;
@@ -541,9 +590,10 @@ bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_
     if (K > 10) return BKMOO_EUNSUPPORTED;
     const int g = refill_grid(K, (int)dt, (int)out_dt);
     if (g <= 0) return BKMOO_EUNSUPPORTED;
-    const HybLayout lay{g - kHybridSolvers, 0, 0, 0};
+    const int groups = refill_groups(K, (int)dt, N, B);
+    const HybLayout lay{(g - refill_solvers(groups)) / groups, 0, 0, 0};
     const int64_t unit = hybrid_unit_elems((int)dt), held_max = refill_held_elems(K, (int)dt);
-    const int64_t smin = (int64_t)g_refill_stream.load() * unit;
+    const int64_t smin = (int64_t)refill_stream_min() * unit;
     uint64_t reread = 0;
     for (int b = 0; b < B; ++b) {  // each segment re-reads what it did not keep
       const int64_t n = offsets_host[b + 1] - offsets_host[b];
@@ -608,13 +658,9 @@ bkmoo_status bkmoo_resolve_path(int32_t K, int64_t N, int32_t B, bkmoo_dtype dt,
   if (st != BKMOO_OK) return st;
   if (!valid_dtype(out_dt) || method < BKMOO_MGDA || method > BKMOO_CAGRAD_EXACT) return BKMOO_EINVAL;
   if (k_unsupported(K, method)) return BKMOO_EUNSUPPORTED;
-  if (choose_refill(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter) > 0)
-    *path = BKMOO_PATH_REFILL;
-  else if (choose_hybrid(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter,
-                         layout(K, N, B, dt).cap_chunks) > 0)
-    *path = BKMOO_PATH_HYBRID;
-  else
-    *path = BKMOO_PATH_TWO_PASS;
+  int grid = 0;
+  *path = pick_path(K, (int)dt, (int)out_dt, N, B, aligned != 0, (int)method, max_iter,
+                    layout(K, N, B, dt).cap_chunks, &grid);
   return BKMOO_OK;
 }
 
@@ -622,12 +668,6 @@ bkmoo_status bkmoo_set_resolve_path(int32_t path) {
   if (path != 0 && path != BKMOO_PATH_TWO_PASS && path != BKMOO_PATH_HYBRID && path != BKMOO_PATH_REFILL)
     return BKMOO_EINVAL;
   g_resolve_path.store(path);
-  return BKMOO_OK;
-}
-
-bkmoo_status bkmoo_set_refill_stream(int32_t vectors) {
-  if (vectors < 0) return BKMOO_EINVAL;
-  g_refill_stream.store(vectors);
   return BKMOO_OK;
 }
 

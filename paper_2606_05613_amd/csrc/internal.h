@@ -11,7 +11,6 @@ constexpr int kMinK = 2;
 constexpr int kMaxK = 16;
 constexpr int kExactMaxK = 10;  // exact solvers: 2^K - 1 supports per bucket
 constexpr int kHybridMaxK = 8;  // the pipelined cooperative resolve (hybrid.hip)
-constexpr int kRefillMaxK = 10; // the single-buffer pipelined resolve (refill.hip)
 constexpr int kThreads = 256;          // streaming kernels: 4 wavefronts of 64
 constexpr int kWave = 64;
 
@@ -224,18 +223,6 @@ hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, con
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
                          uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid,
                          const HybLayout &layout, hipStream_t s);
-
-// Single-buffer pipelined resolve (K <= 4, refill.hip): cooperative grid
-// (0 if it cannot run), elements of a segment it can keep on chip, launch.
-// Its data workgroups hold equal segments; `stream_min` vectors per row and
-// thread of each segment are always streamed.
-int refill_grid(int K, int dt, int out_dt);
-int64_t refill_held_elems(int K, int dt);
-hipError_t launch_refill(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
-                         int shift, int method, int iters, double c, const int8_t *order, double *gram,
-                         float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
-                         uint32_t *recs, uint32_t *err, uint32_t spin_limit, int grid, int stream_min,
-                         hipStream_t s);
 
 int device_cu_count();
 

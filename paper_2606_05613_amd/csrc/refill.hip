@@ -51,6 +51,7 @@
 // workgroup resident.
 #include "combine_impl.h"
 #include "coop_common.h"
+#include "refill.h"
 #include "solve_impl.h"
 
 namespace bkmoo {
@@ -75,6 +76,12 @@ constexpr int ref_regs(int K) {
 constexpr int ref_lds(int K) { return K <= 2 ? 8 : K <= 4 ? 4 : K <= 8 ? 2 : 1; }
 constexpr int ref_stream(int K) { return K <= 7 ? 2 : 1; }
 constexpr int ref_lag(int K) { return K <= 4 ? 2 : 1; }
+// Vectors per row and thread every segment streams rather than keeps: the
+// streamed parts of two buckets are the window that hides a bucket's
+// hand-off (at K <= 4, 2..6 measured alike: the one-bucket loop, not the
+// window, sets the pace there; above K = 4 the kept share is capped by NB
+// first).
+constexpr int kRefStreamMin = 4;
 // Partial entries a solver thread loads at once (16-byte device-coherent
 // loads in flight): all of its share of the slots, at most 24 (registers).
 constexpr int ref_red_batch(int ng) { return (kRefMaxSlotsEst + ng - 1) / ng < 24 ? (kRefMaxSlotsEst + ng - 1) / ng : 24; }
@@ -95,9 +102,9 @@ struct RefArgs {
   uint32_t *recs;    // [kFlagCopies][B] records of K weights at stride kSyncStride, pending-marked
   uint32_t *err;
   uint32_t spin_limit;
-  HybLayout lay;     // segment slots (equal segments)
+  HybLayout lay;     // segment slots of one group (equal segments)
   int nsolv;         // solver workgroups
-  int stream_min;    // vectors per row and thread always streamed (not kept)
+  int groups;        // data workgroup groups: group g takes buckets g, g + groups, ...
 };
 
 // Cache policy of device-coherent loads (sc1, as agent-scope atomic loads).
@@ -181,7 +188,7 @@ struct Refill {
     g.nh = g.has ? sp.nh : 0;
     g.nt = g.has ? sp.nt : 0;
     g.nslot = (g.nv + T - 1) / T;
-    int keep = g.nslot - a.stream_min;
+    int keep = g.nslot - kRefStreamMin;
     g.keep = keep < 0 ? 0 : keep > NB ? NB : keep;
 #pragma unroll
     for (int i = 0; i < K; ++i)
@@ -339,10 +346,20 @@ struct Refill {
     }
   }
 
+  // Parity of bucket b in its group's sequence (selects the partial-slot set
+  // and the LDS copies), and the first partial slot of bucket b's group in
+  // that set: slots [set][group][slot].
+  static __device__ __forceinline__ int par(const RefArgs &a, int b) { return (b / a.groups) & 1; }
+  static __device__ __forceinline__ int64_t slot0(const RefArgs &a, int b) {
+    return ((int64_t)par(a, b) * a.groups + b % a.groups) * a.lay.nslots;
+  }
+
   // Bucket b's partial Gram of this share: fixed-order reductions (xor
   // butterfly in the wave, waves in order), one agent-scope store per entry
-  // into slot `slot` of set b & 1 (all by wavefront 0), then the arrival.
+  // into slot `slot` of its group's set (all by wavefront 0), then the
+  // arrival.
   static __device__ __forceinline__ void arrive(const RefArgs &a, Smem &sm, int b, int slot, float (&acc)[P]) {
+    const int q2 = par(a, b);
     const int t = threadIdx.x, lane = t & (kWave - 1), wave = t / kWave;
 #pragma unroll
     for (int off = kWave / 2; off >= 1; off >>= 1) {
@@ -351,14 +368,14 @@ struct Refill {
     }
     if (lane == 0) {
 #pragma unroll
-      for (int p = 0; p < P; ++p) sm.red[b & 1][wave][p] = (double)acc[p];
+      for (int p = 0; p < P; ++p) sm.red[q2][wave][p] = (double)acc[p];
     }
     __syncthreads();
     if (t < P) {
-      double v = sm.red[b & 1][0][t];
+      double v = sm.red[q2][0][t];
 #pragma unroll
-      for (int q = 1; q < kRefWaves; ++q) v += sm.red[b & 1][q][t];
-      store_agent(&a.partials[((int64_t)(b & 1) * a.lay.nslots + slot) * PP + t], v);
+      for (int q = 1; q < kRefWaves; ++q) v += sm.red[q2][q][t];
+      store_agent(&a.partials[(slot0(a, b) + slot) * PP + t], v);
     }
     if (t == 0) {
       publish_point();  // the slot before the arrival
@@ -374,34 +391,37 @@ struct Refill {
       uint32_t x[K];
       const bool ok = poll_record<K, 32>(a.recs + ((int64_t)(w % kFlagCopies) * a.B + b) * kSyncStride, x, a);
 #pragma unroll
-      for (int i = 0; i < K; ++i) sm.wsh[b & 1][i] = ok ? __uint_as_float(x[i]) : __builtin_nanf("");
+      for (int i = 0; i < K; ++i) sm.wsh[par(a, b)][i] = ok ? __uint_as_float(x[i]) : __builtin_nanf("");
     }
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < K; ++i) wv[i] = sm.wsh[b & 1][i];
+    for (int i = 0; i < K; ++i) wv[i] = sm.wsh[par(a, b)][i];
   }
 
+  // Data workgroup w: group w % groups, slot w / groups of that group's
+  // buckets (none when the grid does not divide evenly).
   static __device__ void data(const Rows<K> &rows, const RefArgs &a, Smem &sm, int w) {
-    const int slot = a.lay.slot(w);
+    const int G = a.groups, grp = w % G, slot = w / G;
+    if (slot >= a.lay.nslots || grp >= a.B) return;
     u32x4 reg[NR][K];
     float hs_cur[K], hs_nxt[K];
 #pragma unroll
     for (int i = 0; i < K; ++i) hs_cur[i] = hs_nxt[i] = 0.0f;
     float acc[P];
-    Geo gn = geo(rows, a, 0, slot);
+    Geo gn = geo(rows, a, grp, slot);
     if (gn.has) {
 #pragma unroll
       for (int p = 0; p < P; ++p) acc[p] = 0.0f;
       stream_in(rows, gn, acc, hs_nxt);
       keep_in(gn, sm, reg, acc);
-      arrive(a, sm, 0, slot, acc);
+      arrive(a, sm, grp, slot, acc);
     }
-    for (int b = 0; b < a.B; ++b) {
+    for (int b = grp; b < a.B; b += G) {
       const Geo gc = gn;
 #pragma unroll
       for (int i = 0; i < K; ++i) hs_cur[i] = hs_nxt[i];
-      if (b + 1 < a.B) {
-        gn = geo(rows, a, b + 1, slot);
+      if (b + G < a.B) {
+        gn = geo(rows, a, b + G, slot);
       } else {
         gn.has = false;
         gn.keep = gn.nslot = gn.nv = gn.nh = gn.nt = 0;
@@ -417,7 +437,7 @@ struct Refill {
       // writes are the slowest traffic) runs at raised wave priority
       __builtin_amdgcn_s_setprio(1);
       refill(a, gc, gn, wv, sm, reg, acc);
-      if (gn.has) arrive(a, sm, b + 1, slot, acc);
+      if (gn.has) arrive(a, sm, b + G, slot, acc);
       if (gc.has) reread(a, gc, wv, hs_cur);
       __builtin_amdgcn_s_setprio(0);
     }
@@ -453,8 +473,7 @@ struct Refill {
       // flight), then each entry sums its groups ascending
       if (t < P2 * NG) {
         const int q = t / NG, g = t % NG;
-        const Rsrc rp = make_rsrc(a.partials + (int64_t)(b & 1) * a.lay.nslots * PP,
-                                  (uint32_t)(a.lay.nslots * PP * 8));
+        const Rsrc rp = make_rsrc(a.partials + slot0(a, b) * PP, (uint32_t)(a.lay.nslots * PP * 8));
         double v0 = 0.0, v1 = 0.0;
         for (int64_t s0 = g; s0 < nseg; s0 += (int64_t)RB * NG) {
           u32x4 x[RB];
@@ -582,7 +601,7 @@ int refill_grid_t() {
       hipSuccess)
     return 0;
   const int g = (occ < 2 ? occ : 2) * device_cu_count();
-  return g > 2 * kHybridSolvers && g - kHybridSolvers <= kRefMaxSlots ? g : 0;
+  return g > 2 * kRefMaxGroups && g - kHybridSolvers <= kRefMaxSlots ? g : 0;
 }
 
 }  // namespace
@@ -607,6 +626,13 @@ int refill_grid(int K, int dt, int out_dt) {
 #undef BKMOO_REF_CASE
 }
 
+int refill_stream_min() { return kRefStreamMin; }
+
+// One solver per group, at least four: solver j takes the buckets of group
+// j (more groups than solvers would queue one group's ready bucket behind
+// another's unfinished one).
+int refill_solvers(int groups) { return groups < kHybridSolvers ? kHybridSolvers : groups; }
+
 int64_t refill_held_elems(int K, int dt) {
   return (int64_t)kRefThreads * (ref_regs(K) + ref_lds(K)) * vec_elems(dt);
 }
@@ -614,12 +640,13 @@ int64_t refill_held_elems(int K, int dt) {
 hipError_t launch_refill(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
                          int shift, int method, int iters, double c, const int8_t *order, double *gram,
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
-                         uint32_t *recs, uint32_t *err, uint32_t spin_limit, int grid, int stream_min,
+                         uint32_t *recs, uint32_t *err, uint32_t spin_limit, int grid, int groups,
                          hipStream_t s) {
-  const int nsolv = kHybridSolvers;
-  const HybLayout lay{grid - nsolv, 0, 0, 0};
+  const int nsolv = refill_solvers(groups);
+  if (groups < 1 || grid - nsolv < groups) return hipErrorInvalidValue;
+  const HybLayout lay{(grid - nsolv) / groups, 0, 0, 0};
   const RefArgs a{offs, B, shift, method, iters, c, order, gram, weights, aux, out, partials, arrive, recs,
-                  err, spin_limit, lay, nsolv, stream_min};
+                  err, spin_limit, lay, nsolv, groups};
   hipLaunchKernelGGL(refill_init_kernel, dim3(64), dim3(256), 0, s, arrive, (int64_t)B * kSyncStride, recs,
                      (int64_t)kFlagCopies * B * kSyncStride);
   hipError_t e = hipGetLastError();

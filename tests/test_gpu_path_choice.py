@@ -1,10 +1,14 @@
 """The automatic choice between the resolve paths (bkmoo_resolve_path) on
-MI355X shapes: the hybrid path (K <= 8) needs at least 8 buckets, at least
+MI355X shapes.  The hybrid path (K <= 8) needs at least 8 buckets, at least
 10% of a bucket kept on chip, and buckets (all K rows) of at least
-max(24, 6 K) MiB plus 4 MiB per microsecond of estimated solve latency (0.07 K us per MGDA and
-0.22 K us per CAGrad iteration, 0.1 K^2 us for PCGrad); everything else
-runs the two passes.  Only shapes are used (no resolve runs); the cases sit away from
-the thresholds."""
+max(24, 6 K) MiB plus 4 MiB per microsecond of estimated solve latency L
+(0.07 K us per MGDA and 0.22 K us per CAGrad iteration, 0.1 K^2 us for
+PCGrad).  The refill path (K <= 10) needs at least 8 buckets and a round of
+its G = clamp(round(180 MiB / bucket), 1, 32) groups' buckets between
+64 + 2 L and 300 MiB; it runs where the hybrid path does not, and instead
+of it for K <= 4 with L >= 10 us.  Everything else runs the two passes.
+Only shapes are used (no resolve runs); the cases sit away from the
+thresholds."""
 
 import pytest
 import torch
@@ -22,20 +26,20 @@ def rows_4x2g():
 
 # (buckets, method, iterations, expected path name); rows of 512 MiB
 CASES_4x2G = [
-    (8, "mgda", 20, "hybrid"),       # 256 MiB buckets (all rows) >= 24 + 4 * 5.6
-    (8, "mgda", 100, "hybrid"),      # >= 24 + 4 * 28
-    (8, "cagrad", 20, "hybrid"),     # >= 24 + 4 * 17.6
-    (8, "cagrad", 100, "two-pass"),  # < 24 + 4 * 88
+    (8, "mgda", 20, "hybrid"),       # 256 MiB buckets (all rows) >= 24 + 4 * 5.6; L < 10
+    (8, "mgda", 100, "refill"),      # both run (256 >= 24 + 4 * 28, G = 1); L = 28 >= 10
+    (8, "cagrad", 20, "refill"),     # both run; L = 17.6 >= 10
+    (8, "cagrad", 100, "refill"),    # hybrid: 256 < 24 + 4 * 88; refill: 256 >= 64 + 2 * 88
     (8, "pcgrad", 0, "hybrid"),
     (8, "mean", 0, "hybrid"),
     (32, "mgda", 20, "hybrid"),      # 64 MiB
-    (32, "mgda", 100, "two-pass"),
-    (32, "cagrad", 20, "two-pass"),
-    (48, "mgda", 20, "two-pass"),    # 42.7 MiB < 46.4
+    (32, "mgda", 100, "refill"),     # hybrid 64 < 136; G = 3, round 192 >= 120
+    (32, "cagrad", 20, "refill"),    # hybrid 64 < 94.4; round 192 >= 99.2
+    (48, "mgda", 20, "refill"),      # hybrid 42.7 MiB < 46.4; G = 4, round 171
     (48, "mean", 0, "hybrid"),
     (64, "mean", 0, "hybrid"),       # 32 MiB
-    (64, "mgda", 20, "two-pass"),
-    (96, "mean", 0, "two-pass"),     # 21.3 MiB < 24
+    (64, "mgda", 20, "refill"),      # hybrid 32 < 46.4; G = 6, round 192
+    (96, "mean", 0, "refill"),       # hybrid 21.3 MiB < 24; G = 8, round 171
     (4, "mean", 0, "two-pass"),      # fewer than 8 buckets
     (8, "mgda-exact", 0, "two-pass"),
 ]
@@ -43,7 +47,7 @@ CASES_4x2G = [
 
 @pytest.mark.parametrize("B,method,iters,want", CASES_4x2G)
 def test_automatic_path(gpu_lib, rows_4x2g, B, method, iters, want):
-    names = {gpu_lib.PATH_TWO_PASS: "two-pass", gpu_lib.PATH_HYBRID: "hybrid"}
+    names = {gpu_lib.PATH_TWO_PASS: "two-pass", gpu_lib.PATH_HYBRID: "hybrid", gpu_lib.PATH_REFILL: "refill"}
     gpu_lib.set_resolve_path(0)
     got = names[gpu_lib.resolve_path(rows_4x2g, B + 1, method, iters)]
     assert got == want, f"B={B} {method}-{iters}: {got}"
@@ -51,26 +55,27 @@ def test_automatic_path(gpu_lib, rows_4x2g, B, method, iters, want):
 
 # (K, buckets, method, iterations, expected path name); rows of 2^28 bf16
 # elements (512 MiB).  Each case's side was measured on MI355X: at K = 8
-# the pipelined kernel loses at 4 MiB per row, wins at 8-25 MiB when the
-# solve is short enough, and keeps too little on chip at 50 MiB.
+# the two-buffer kernel loses at 4 MiB per row, wins at 8-25 MiB when the
+# solve is short enough, and keeps too little on chip at 50 MiB; grouped
+# buckets on the refill kernel take the smaller buckets.
 CASES_MORE_TASKS = [
-    (8, 128, "mean", 0, "two-pass"),   # 32 MiB buckets < 48 (6 MiB per row)
+    (8, 128, "mean", 0, "refill"),     # hybrid: 32 MiB < 48 (6 MiB per row); G = 6, round 192
     (8, 64, "mean", 0, "hybrid"),      # 64 MiB >= 48
-    (8, 64, "mgda", 20, "two-pass"),   # 64 < 48 + 4 * 11.2
+    (8, 64, "mgda", 20, "refill"),     # hybrid 64 < 48 + 4 * 11.2; G = 3, round 192 >= 86.4
     (8, 32, "mgda", 20, "hybrid"),     # 128 >= 92.8
     (8, 32, "pcgrad", 0, "hybrid"),    # 128 >= 48 + 4 * 6.4
-    (8, 32, "cagrad", 20, "two-pass"), # 128 < 48 + 4 * 35.2
+    (8, 32, "cagrad", 20, "two-pass"), # hybrid 128 < 48 + 4 * 35.2; G = 1, round 128 < 64 + 2 * 35.2
     (8, 20, "cagrad", 20, "hybrid"),   # 204.8 >= 188.8
-    (8, 10, "mean", 0, "two-pass"),    # 51 MiB per row: < 10% kept on chip
+    (8, 10, "mean", 0, "two-pass"),    # 51 MiB per row: < 10% kept on chip; round 410 > 300
     (6, 64, "mean", 0, "hybrid"),      # 48 MiB >= 36
-    (6, 128, "mean", 0, "two-pass"),   # 24 MiB < 36
+    (6, 128, "mean", 0, "refill"),     # hybrid 24 MiB < 36; G = 8, round 192
     (5, 32, "mgda", 20, "hybrid"),     # 80 MiB >= 30 + 4 * 7
 ]
 
 
 @pytest.mark.parametrize("K,B,method,iters,want", CASES_MORE_TASKS)
 def test_automatic_path_more_tasks(gpu_lib, K, B, method, iters, want):
-    names = {gpu_lib.PATH_TWO_PASS: "two-pass", gpu_lib.PATH_HYBRID: "hybrid"}
+    names = {gpu_lib.PATH_TWO_PASS: "two-pass", gpu_lib.PATH_HYBRID: "hybrid", gpu_lib.PATH_REFILL: "refill"}
     g = torch.empty((K, 1 << 28), dtype=torch.bfloat16, device="cuda")
     gpu_lib.set_resolve_path(0)
     got = names[gpu_lib.resolve_path(g, B + 1, method, iters)]
