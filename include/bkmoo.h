@@ -238,16 +238,21 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  *             keeps up to twice the hybrid's share of each bucket on chip
  *             in a single buffer: the part of bucket b+1 it does not keep
  *             is read while bucket b is solved, then each kept vector of
- *             bucket b is combined and replaced by bucket b+1's.  Rounding,
- *             determinism and bounded waits as for hybrid.
- * Automatic choice: for K <= 8 the hybrid path for at least 8 buckets of
- * which at least 10% stays on chip, averaging (all K rows) at least
- * max(24, 6 K) MiB plus 4 MiB per microsecond of estimated solve latency
- * (0.07 K us per MGDA iteration, 0.22 K us per CAGrad iteration, 0.1 K^2 us
- * for PCGrad, 0 for the mean), so that each bucket's hand-off is amortised;
- * for K = 9, 10 the refill path under the same size rule without the
- * on-chip share; else the two passes.  Exact solvers never take a
- * cooperative path.
+ *             bucket b is combined and replaced by bucket b+1's.  Its data
+ *             workgroups form G groups (G = clamp(round(180 MiB / bucket
+ *             size, all rows), 1, 32), at most B) and group g takes buckets
+ *             g, g+G, ..., so small buckets hide their hand-off too.
+ *             Rounding, determinism and bounded waits as for hybrid (its
+ *             segments also depend on G).
+ * Automatic choice, with L the estimated solve latency (0.07 K us per MGDA
+ * iteration, 0.22 K us per CAGrad iteration, 0.1 K^2 us for PCGrad, 0 for
+ * the mean): hybrid (K <= 8) is eligible for at least 8 buckets of which at
+ * least 10% stays on chip, averaging (all K rows) at least max(24, 6 K) MiB
+ * plus 4 MiB per us of L; refill (K <= 10) for at least 8 buckets whose
+ * round of G buckets holds between 64 + 2 L and 300 MiB.  Hybrid where it
+ * is eligible, except refill for K <= 4 with L >= 10 us; else refill where
+ * eligible; else the two passes.  Exact solvers never take a cooperative
+ * path.
  * bkmoo_resolve_path reports the choice; bkmoo_set_resolve_path forces one.
  */
 bkmoo_status bkmoo_resolve(int32_t K, const void *const *grads, bkmoo_dtype dt, int64_t N, int32_t B,

@@ -504,7 +504,8 @@ bkmoo_status resolve_impl(int32_t K, const void *const *grads, bkmoo_dtype dt, i
     if (e != hipSuccess) return BKMOO_EHIP;
     e = launch_refill(K, (int)dt, (int)out_dt, grads, bucket_offsets, B, shift, (int)method, iters, c, order,
                       G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride, w.err, g_spin_limit.load(),
-                      pgrid, refill_groups(K, (int)dt, N, B), stream);
+                      pgrid, refill_groups(K, (int)dt, N, B),
+                      refill_temporal_slots(K, (int)dt, pgrid, refill_groups(K, (int)dt, N, B)), stream);
     return hip_status(e);
   }
   if (path == BKMOO_PATH_HYBRID) {

@@ -16,6 +16,9 @@ constexpr int kRefMaxGroups = 32;  // bucket groups (and solvers) at most
 int refill_grid(int K, int dt, int out_dt);
 int64_t refill_held_elems(int K, int dt);
 int refill_stream_min();
+// Streamed vectors per row and thread a data workgroup reads with the
+// temporal cache policy, for `groups` groups over a grid of `grid`.
+int refill_temporal_slots(int K, int dt, int grid, int groups);
 // Solver workgroups for `groups` groups of data workgroups: group g takes
 // buckets g, g + groups, ..., each spread over (grid - solvers) / groups
 // data workgroups.
@@ -24,6 +27,6 @@ hipError_t launch_refill(int K, int dt, int out_dt, const void *const *rows, con
                          int shift, int method, int iters, double c, const int8_t *order, double *gram,
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
                          uint32_t *recs, uint32_t *err, uint32_t spin_limit, int grid, int groups,
-                         hipStream_t s);
+                         int tslots, hipStream_t s);
 
 }  // namespace bkmoo

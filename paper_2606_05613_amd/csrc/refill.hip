@@ -82,6 +82,12 @@ constexpr int ref_lag(int K) { return K <= 4 ? 2 : 1; }
 // window, sets the pace there; above K = 4 the kept share is capped by NB
 // first).
 constexpr int kRefStreamMin = 4;
+// Streamed bytes per round read with the temporal policy.  K=10 fp32, 25
+// MiB per row (263 buckets, one group), CAGrad FW-20, ms: all 11 streamed
+// vectors per row temporal 22.23, 8 (166 MB a round) 20.58, 5 20.97, 3
+// 21.60, none 23.45; 5 and 1 MiB per row (their whole streamed part, 183
+// and 117 MB a round) lose 0.3-1 ms with fewer.
+constexpr double kRefTemporalMiB = 170.0;
 // Partial entries a solver thread loads at once (16-byte device-coherent
 // loads in flight): all of its share of the slots, at most 24 (registers).
 constexpr int ref_red_batch(int ng) { return (kRefMaxSlotsEst + ng - 1) / ng < 24 ? (kRefMaxSlotsEst + ng - 1) / ng : 24; }
@@ -105,6 +111,7 @@ struct RefArgs {
   HybLayout lay;     // segment slots of one group (equal segments)
   int nsolv;         // solver workgroups
   int groups;        // data workgroup groups: group g takes buckets g, g + groups, ...
+  int tslots;        // streamed vectors per row and thread read with the temporal policy (the rest streaming)
 };
 
 // Cache policy of device-coherent loads (sc1, as agent-scope atomic loads).
@@ -226,8 +233,11 @@ struct Refill {
   }
 
   // The scalar head and tail elements (held in hs) and the streamed
-  // vectors [keep, nslot) of a share: Gram sums only.
-  static __device__ __forceinline__ void stream_in(const Rows<K> &rows, const Geo &g, float (&acc)[P],
+  // vectors [keep, nslot) of a share: Gram sums only.  The first `tslots`
+  // are read with the temporal policy, so that their second read (C2) finds
+  // them in the last-level cache; the rest with the streaming policy, so
+  // that they do not push those out.
+  static __device__ __forceinline__ void stream_in(const Rows<K> &rows, const Geo &g, int tslots, float (&acc)[P],
                                                    float (&hs)[K]) {
     const int t = threadIdx.x;
     if (t < g.nh + g.nt) {
@@ -237,12 +247,24 @@ struct Refill {
       accumulate<K>(acc, hs);
     }
     const uint32_t voff = (uint32_t)t * 16u;
-    for (int j0 = g.keep; j0 < g.nslot; j0 += NS) {
+    const int jt = g.keep + tslots < g.nslot ? g.keep + tslots : g.nslot;
+    int j0 = g.keep;
+    for (; j0 < jt; j0 += NS) {
       u32x4 q[NS][K];
 #pragma unroll
       for (int u = 0; u < NS; ++u) {
 #pragma unroll
         for (int i = 0; i < K; ++i) q[u][i] = buf_load16_keep(g.rs[i], voff, (uint32_t)((j0 + u) * T * 16));
+      }
+#pragma unroll
+      for (int u = 0; u < NS; ++u) accumulate_vec(acc, q[u]);
+    }
+    for (; j0 < g.nslot; j0 += NS) {
+      u32x4 q[NS][K];
+#pragma unroll
+      for (int u = 0; u < NS; ++u) {
+#pragma unroll
+        for (int i = 0; i < K; ++i) q[u][i] = buf_load16(g.rs[i], voff, (uint32_t)((j0 + u) * T * 16));
       }
 #pragma unroll
       for (int u = 0; u < NS; ++u) accumulate_vec(acc, q[u]);
@@ -412,7 +434,7 @@ struct Refill {
     if (gn.has) {
 #pragma unroll
       for (int p = 0; p < P; ++p) acc[p] = 0.0f;
-      stream_in(rows, gn, acc, hs_nxt);
+      stream_in(rows, gn, a.tslots, acc, hs_nxt);
       keep_in(gn, sm, reg, acc);
       arrive(a, sm, grp, slot, acc);
     }
@@ -428,7 +450,7 @@ struct Refill {
       }
 #pragma unroll
       for (int p = 0; p < P; ++p) acc[p] = 0.0f;
-      if (gn.has) stream_in(rows, gn, acc, hs_nxt);
+      if (gn.has) stream_in(rows, gn, a.tslots, acc, hs_nxt);
       float wv[K];
 #pragma unroll
       for (int i = 0; i < K; ++i) wv[i] = 0.0f;
@@ -628,6 +650,16 @@ int refill_grid(int K, int dt, int out_dt) {
 
 int refill_stream_min() { return kRefStreamMin; }
 
+// The streamed part a round of the groups' buckets leaves in the last-level
+// cache for its second read: at most kRefTemporalMiB over all data
+// workgroups (one round's is re-read while the next round's is read).
+int refill_temporal_slots(int K, int dt, int grid, int groups) {
+  const int nsolv = refill_solvers(groups);
+  const double per_slot = (double)(grid - nsolv) * kRefThreads * 16.0 * K;  // one vector per row and thread
+  const int t = (int)(kRefTemporalMiB * (1 << 20) / per_slot);
+  return t < 0 ? 0 : t;
+}
+
 // One solver per group, at least four: solver j takes the buckets of group
 // j (more groups than solvers would queue one group's ready bucket behind
 // another's unfinished one).
@@ -641,12 +673,12 @@ hipError_t launch_refill(int K, int dt, int out_dt, const void *const *rows, con
                          int shift, int method, int iters, double c, const int8_t *order, double *gram,
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
                          uint32_t *recs, uint32_t *err, uint32_t spin_limit, int grid, int groups,
-                         hipStream_t s) {
+                         int tslots, hipStream_t s) {
   const int nsolv = refill_solvers(groups);
   if (groups < 1 || grid - nsolv < groups) return hipErrorInvalidValue;
   const HybLayout lay{(grid - nsolv) / groups, 0, 0, 0};
   const RefArgs a{offs, B, shift, method, iters, c, order, gram, weights, aux, out, partials, arrive, recs,
-                  err, spin_limit, lay, nsolv, groups};
+                  err, spin_limit, lay, nsolv, groups, tslots};
   hipLaunchKernelGGL(refill_init_kernel, dim3(64), dim3(256), 0, s, arrive, (int64_t)B * kSyncStride, recs,
                      (int64_t)kFlagCopies * B * kSyncStride);
   hipError_t e = hipGetLastError();
