@@ -288,11 +288,17 @@ constexpr double kRefillMaxRoundMiB = 300.0;
 // per microsecond of estimated solve latency.
 constexpr double kRefillMinRoundMiB = 64.0, kRefillMiBPerUs = 2.0;
 // Where both cooperative kernels can run (K <= 8, large buckets) the
-// two-buffer one is as fast or faster except for long solves at K <= 4
-// (25 MiB per row, bf16, ms, two-buffer / refill: K=4 CAGrad FW-20 18.96 /
-// 16.85 (G=2), MGDA FW-20 17.31 / 17.15, PCGrad 16.06 / 17.17; K=8 CAGrad
-// FW-20 36.4 / 39.4 (G=1), 41.0 (G=2); K=6 MGDA 3.42 / 3.75).
-constexpr double kRefillOverHybridUs = 10.0;
+// two-buffer one is as fast or faster at K > 4 and for short solves; at
+// K <= 4 a solve of a few microseconds shows in its hand-off, while the
+// refill kernel's groups hide it.  Measured on MI355X, bf16, ms, two-buffer
+// / refill at the rule's G: K=4 25 MiB per row (613 buckets) MGDA FW-20
+// 17.36 / 16.82 (G=2), CAGrad FW-20 19.02 / 16.70, mean 16.06 / 17.02,
+// PCGrad 16.09 / 17.06; K=4 50 MiB (82) MGDA 5.34 / 4.98 (G=1), CAGrad
+// 5.24 / 5.02; K=4 12.5 MiB (328) MGDA 5.66 / 4.52 (G=4); K=3 25 MiB (328)
+// MGDA 5.24 / 4.79 (G=2), CAGrad 5.48 / 5.04; K=2 25 MiB (328) MGDA FW-20
+// (2.8 us) 5.52 / 5.83 (G=4), CAGrad 6.83 / 5.70; K=6 MGDA 3.42 / 3.75; K=8
+// CAGrad FW-20 36.4 / 39.4 (G=1), 41.0 (G=2).
+constexpr double kRefillOverHybridUs = 4.0;
 
 int refill_groups(int K, int dt, int64_t N, int B) {
   const double bucket_mib = (double)N / B * K * elem_bytes(dt) / (1 << 20);

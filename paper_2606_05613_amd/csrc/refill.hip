@@ -70,12 +70,15 @@ constexpr uint32_t kWeightPending = 0x7f800001u;
 // streamed per row and step (NS), and kept slots between a refill load and
 // the addition of its products (lag): the registers and LDS the two-buffer
 // kernel spreads over two buckets, as far as they compile without spills.
+// At K = 4 one more kept register vector with a lag of one slot beat seven
+// with a lag of two (K=4 bf16 25 MiB MGDA FW-20, two groups: 16.82-16.92
+// against 17.13-17.18 ms).
 constexpr int ref_regs(int K) {
-  return K <= 2 ? 16 : K == 3 ? 10 : K == 4 ? 7 : K == 5 ? 4 : K == 6 ? 3 : K <= 8 ? 2 : 1;
+  return K <= 2 ? 16 : K == 3 ? 10 : K == 4 ? 8 : K == 5 ? 4 : K == 6 ? 3 : K <= 8 ? 2 : 1;
 }
 constexpr int ref_lds(int K) { return K <= 2 ? 8 : K <= 4 ? 4 : K <= 8 ? 2 : 1; }
 constexpr int ref_stream(int K) { return K <= 7 ? 2 : 1; }
-constexpr int ref_lag(int K) { return K <= 4 ? 2 : 1; }
+constexpr int ref_lag(int K) { return K <= 3 ? 2 : 1; }
 // Vectors per row and thread every segment streams rather than keeps: the
 // streamed parts of two buckets are the window that hides a bucket's
 // hand-off (at K <= 4, 2..6 measured alike: the one-bucket loop, not the

@@ -174,7 +174,7 @@ def _check_workload(lib, wl, grads, offs, order, gram_cache=None):
 
 # the path bkmoo_resolve takes for each workload (what bench.py times)
 EXPECTED_PATH = {"k2-mgda-1m-f32": "PATH_TWO_PASS", "gpt2-124m-k4-pcgrad-f32": "PATH_HYBRID",
-                 "llama3-8b-k4-mgda-bf16": "PATH_HYBRID", "llama3-8b-k8-cagrad-bf16": "PATH_HYBRID"}
+                 "llama3-8b-k4-mgda-bf16": "PATH_REFILL", "llama3-8b-k8-cagrad-bf16": "PATH_HYBRID"}
 
 
 @pytest.mark.parametrize("name", list(EXPECTED_PATH))

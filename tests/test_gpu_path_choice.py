@@ -6,7 +6,7 @@ max(24, 6 K) MiB plus 4 MiB per microsecond of estimated solve latency L
 PCGrad).  The refill path (K <= 10) needs at least 8 buckets and a round of
 its G = clamp(round(180 MiB / bucket), 1, 32) groups' buckets between
 64 + 2 L and 300 MiB; it runs where the hybrid path does not, and instead
-of it for K <= 4 with L >= 10 us.  Everything else runs the two passes.
+of it for K <= 4 with L >= 4 us.  Everything else runs the two passes.
 Only shapes are used (no resolve runs); the cases sit away from the
 thresholds."""
 
@@ -26,13 +26,15 @@ def rows_4x2g():
 
 # (buckets, method, iterations, expected path name); rows of 512 MiB
 CASES_4x2G = [
-    (8, "mgda", 20, "hybrid"),       # 256 MiB buckets (all rows) >= 24 + 4 * 5.6; L < 10
-    (8, "mgda", 100, "refill"),      # both run (256 >= 24 + 4 * 28, G = 1); L = 28 >= 10
-    (8, "cagrad", 20, "refill"),     # both run; L = 17.6 >= 10
+    (8, "mgda", 20, "refill"),       # both run (256 MiB buckets (all rows) >= 24 + 4 * 5.6, G = 1); L >= 4
+    (8, "mgda", 5, "hybrid"),        # both run; L = 1.4 < 4
+    (8, "mgda", 100, "refill"),      # both run (256 >= 24 + 4 * 28); L = 28
+    (8, "cagrad", 20, "refill"),     # both run; L = 17.6
     (8, "cagrad", 100, "refill"),    # hybrid: 256 < 24 + 4 * 88; refill: 256 >= 64 + 2 * 88
     (8, "pcgrad", 0, "hybrid"),
     (8, "mean", 0, "hybrid"),
-    (32, "mgda", 20, "hybrid"),      # 64 MiB
+    (32, "mgda", 20, "refill"),      # 64 MiB: both run (G = 3, round 192); L = 5.6 >= 4
+    (32, "mgda", 10, "hybrid"),      # both run; L = 2.8 < 4
     (32, "mgda", 100, "refill"),     # hybrid 64 < 136; G = 3, round 192 >= 120
     (32, "cagrad", 20, "refill"),    # hybrid 64 < 94.4; round 192 >= 99.2
     (48, "mgda", 20, "refill"),      # hybrid 42.7 MiB < 46.4; G = 4, round 171

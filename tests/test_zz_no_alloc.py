@@ -3,8 +3,8 @@ device scratch instead of a caller's workspace) against bkmoo_resolve on the
 same inputs, through the C ABI: equal Gram matrices, weights, method
 variables and update, bit for bit, for consecutive calls on the shared
 scratch (each later call on a different and partly smaller input, so
-leftovers of the previous call in the scratch would show), on the hybrid
-and on the two-pass path."""
+leftovers of the previous call in the scratch would show), on the two
+cooperative paths and on the two-pass path."""
 
 import pytest
 import torch
@@ -70,6 +70,16 @@ def test_noalloc_equals_resolve_on_consecutive_calls(gpu_lib):
     # 4: the second case again, now after a larger call
     print("case noalloc 4: case 2 again", flush=True)
     _both(lib, wl2, lib.PATH_TWO_PASS)
+    # 5: K=10 fp32 MGDA on the single-buffer path (bucket groups), then case 1
+    #    on that path after it
+    lens = [120_000, 64_001, 0, 200_000, 33_333, 150_000, 90_000, 111_111, 76_543, 88_888]
+    lens[-1] += -sum(lens) % 4
+    wl5 = small_workload(WORKLOADS["gpt2-124m-k4-pcgrad-f32"], sum(lens), bucket_lens=lens, K=10, dtype="f32",
+                         method="mgda", seed=8105)
+    print(f"case noalloc 5: K=10 f32 mgda B={wl5.B} N={wl5.N} refill", flush=True)
+    _both(lib, wl5, lib.PATH_REFILL)
+    print("case noalloc 6: case 1 on the refill path", flush=True)
+    _both(lib, wl1, lib.PATH_REFILL)
 
 
 def test_noalloc_needs_an_output(gpu_lib):
