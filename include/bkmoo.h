@@ -249,7 +249,8 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  * the mean): hybrid (K <= 8) is eligible for at least 8 buckets of which at
  * least 10% stays on chip, averaging (all K rows) at least max(24, 6 K) MiB
  * plus 4 MiB per us of L; refill (K <= 10) for at least 8 buckets whose
- * round of G buckets holds between 64 + 2 L and 300 MiB.  Hybrid where it
+ * round of G buckets holds at least 64 + 2 L MiB and, for G > 1, at most
+ * 300 MiB (a round the Infinity Cache still serves).  Hybrid where it
  * is eligible, except refill for K <= 4 with L >= 4 us; else refill where
  * eligible; else the two passes.  Exact solvers never take a cooperative
  * path.

@@ -277,11 +277,17 @@ int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
 // 25.3 / 18.6 (G=18; 14: 18.6, 22: 22.5, 8: 33.6), MGDA 25.1 / 18.5,
 // PCGrad 25.1 / 18.3; 5 MiB CAGrad 23.2 / 18.1 (G=4; 3: 19.9, 5: 20.1),
 // MGDA 22.7 / 18.2, PCGrad 22.7 / 17.9; 25 MiB CAGrad 25.1 / 22.3 (G=1;
-// 2: 25.7); 100 MiB (G=1, a 1 GB round) 25.2 / 26.2.  K=4 bf16 2.1B
+// 2: 25.7); 100 MiB (G=1, a 1 GB round) 25.1 / 24.7.  K=4 bf16 2.1B
 // elements, 1 MiB MGDA 6.6 / 4.5 (G=32), CAGrad 6.7 / 5.1; 5 MiB MGDA
 // 6.6 / 4.5 (G=9; 6: 4.3), CAGrad 6.6 / 4.7.  K=8 bf16 1.07B elements,
 // 1 MiB MGDA 6.3 / 4.9 (G=24), CAGrad 6.3 / 5.0; 5 MiB MGDA 6.3 / 4.9
-// (G=4), CAGrad 6.3 / 5.3.
+// (G=4), CAGrad 6.3 / 5.3.  With one group (a bucket of more than ~120
+// MiB) the cap does not apply: the re-read part of a bucket misses as it
+// does on the two passes, and the kept part still saves its second read.
+// Two passes / refill, MGDA FW-20: K=4 bf16 100 MiB per row 6.57 / 5.75,
+// K=4 fp32 400 MiB 3.32 / 3.21, K=2 bf16 400 MiB 3.70 / 3.59, K=6 bf16
+// 100 MiB 4.78 / 4.65, K=8 bf16 100 MiB 6.32 / 6.26, K=9 fp32 100 MiB
+// 3.92 / 3.40, K=10 bf16 100 MiB 8.54 / 8.04 (CAGrad and the mean alike).
 constexpr double kRefillRoundMiB = 180.0;
 constexpr double kRefillMaxRoundMiB = 300.0;
 // A round must also cover the hand-off: at least this much, plus this much
@@ -325,7 +331,7 @@ int choose_refill(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
   if (B < kHybridMinBuckets) return 0;
   const double round_mib = (double)N / B * K * elem_bytes(dt) / (1 << 20) * groups;
   const double min_mib = kRefillMinRoundMiB + kRefillMiBPerUs * solve_latency_us(method, K, iters);
-  return round_mib >= min_mib && round_mib <= kRefillMaxRoundMiB ? g : 0;
+  return round_mib >= min_mib && (round_mib <= kRefillMaxRoundMiB || groups == 1) ? g : 0;
 }
 
 // The path bkmoo_resolve takes and its grid (0 for the two passes).

@@ -202,10 +202,9 @@ def test_full_qwen_k10_bucket_sweep(gpu_lib, mib):
     grads = fill_grads(base, device="cuda")
     offs = torch.from_numpy(base.offsets()).cuda()
     gpu_lib.set_resolve_path(0)
-    # 1-25 MiB buckets take the single-buffer cooperative kernel (1 and 5 MiB
-    # in groups of 18 and 4 buckets), 100 MiB ones the two passes (a 1 GB
-    # bucket's streamed part is not re-read from the last-level cache)
-    want = gpu_lib.PATH_REFILL if mib <= 25 else gpu_lib.PATH_TWO_PASS
+    # every size takes the single-buffer cooperative kernel: 1 and 5 MiB
+    # buckets in groups of 18 and 4, 25 and 100 MiB ones one at a time
+    want = gpu_lib.PATH_REFILL
     for m in ("mgda", "pcgrad", "cagrad"):
         assert gpu_lib.resolve_path(grads, base.B + 1, m, 20 if m != "pcgrad" else 0) == want, (mib, m)
     try:

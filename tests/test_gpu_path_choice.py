@@ -4,8 +4,9 @@ MI355X shapes.  The hybrid path (K <= 8) needs at least 8 buckets, at least
 max(24, 6 K) MiB plus 4 MiB per microsecond of estimated solve latency L
 (0.07 K us per MGDA and 0.22 K us per CAGrad iteration, 0.1 K^2 us for
 PCGrad).  The refill path (K <= 10) needs at least 8 buckets and a round of
-its G = clamp(round(180 MiB / bucket), 1, 32) groups' buckets between
-64 + 2 L and 300 MiB; it runs where the hybrid path does not, and instead
+its G = clamp(round(180 MiB / bucket), 1, 32) groups' buckets of at least
+64 + 2 L MiB and, with more than one group, at most 300 MiB; it runs where
+the hybrid path does not, and instead
 of it for K <= 4 with L >= 4 us.  Everything else runs the two passes.
 Only shapes are used (no resolve runs); the cases sit away from the
 thresholds."""
@@ -68,7 +69,7 @@ CASES_MORE_TASKS = [
     (8, 32, "pcgrad", 0, "hybrid"),    # 128 >= 48 + 4 * 6.4
     (8, 32, "cagrad", 20, "two-pass"), # hybrid 128 < 48 + 4 * 35.2; G = 1, round 128 < 64 + 2 * 35.2
     (8, 20, "cagrad", 20, "hybrid"),   # 204.8 >= 188.8
-    (8, 10, "mean", 0, "two-pass"),    # 51 MiB per row: < 10% kept on chip; round 410 > 300
+    (8, 10, "mean", 0, "refill"),      # 51 MiB per row: hybrid keeps < 10%; G = 1, round 410 (no cap)
     (6, 64, "mean", 0, "hybrid"),      # 48 MiB >= 36
     (6, 128, "mean", 0, "refill"),     # hybrid 24 MiB < 36; G = 8, round 192
     (5, 32, "mgda", 20, "hybrid"),     # 80 MiB >= 30 + 4 * 7
@@ -105,11 +106,14 @@ def test_more_than_eight_tasks(gpu_lib):
 
 def test_hybrid_needs_a_tenth_on_chip(gpu_lib):
     """K=4 bf16, 2^30 elements in 8 buckets of 256 MiB per row: about 5% of
-    each bucket fits on chip, so the two passes run."""
+    each bucket fits in the two-buffer kernel, so the single-buffer one takes
+    the buckets one at a time (a 1 GiB round, beyond the cache, is allowed
+    with one group); with 32 buckets (64 MiB per row, ~19% kept) the
+    two-buffer kernel runs."""
     g = torch.empty((4, 1 << 30), dtype=torch.bfloat16, device="cuda")
     gpu_lib.set_resolve_path(0)
-    assert gpu_lib.resolve_path(g, 9, "mean", 0) == gpu_lib.PATH_TWO_PASS
-    assert gpu_lib.resolve_path(g, 33, "mean", 0) == gpu_lib.PATH_HYBRID  # 64 MiB per row: ~19%
+    assert gpu_lib.resolve_path(g, 9, "mean", 0) == gpu_lib.PATH_REFILL
+    assert gpu_lib.resolve_path(g, 33, "mean", 0) == gpu_lib.PATH_HYBRID
 
 
 def test_misaligned_rows_take_the_two_passes(gpu_lib):
