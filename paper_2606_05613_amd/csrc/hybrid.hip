@@ -34,9 +34,10 @@
 // from a second read of the streamed part.  A wait that runs out sets the
 // error word's timeout bit and the bucket's weights (solver) or the
 // workgroup's copy of them (data workgroup) become NaN, so the call ends and
-// the affected update is NaN instead of silently wrong.  The Gram phase reads the
-// streamed part with the temporal cache policy, so that second read mostly
-// hits the Infinity Cache; solver waves, and data waves in a combine phase,
+// the affected update is NaN instead of silently wrong.  The Gram phase reads
+// the first ~170 MiB of a bucket's streamed part with the temporal cache
+// policy, so that second read mostly hits the Infinity Cache, and the rest
+// with the streaming one; solver waves, and data waves in a combine phase,
 // run at raised wave priority.
 //
 // No cycle of waits: a data workgroup waits for bucket b's weights only after
@@ -81,6 +82,13 @@ constexpr int kHybRedBatch = 24;
 constexpr int hyb_regs(int K) { return K <= 2 ? 9 : K == 3 ? 6 : K == 4 ? 4 : K <= 6 ? 2 : 1; }
 constexpr int hyb_lds(int K) { return K <= 2 ? 4 : K <= 4 ? 2 : 1; }
 constexpr int hyb_stream(int K) { return K <= 7 ? 2 : 1; }
+// Streamed bytes per bucket (all data workgroups) read with the temporal
+// policy.  Llama-3-8B-shaped K=8 bf16, 25 MiB per row (11 streamed vectors
+// per row and thread), ms, CAGrad FW-20 / mean: all temporal 37.10 / 37.55,
+// 10 (166 MB) 36.67 / 35.91, 9 36.77 / 35.61, 8 37.05 / 35.62, 7 37.36 /
+// 35.97, 5 38.5 / 37.7, none 43.5.  K=4 (at most ~70 MB streamed) is fastest
+// with all of it temporal (4-8 of its vectors: 0.7-1.6 ms slower).
+constexpr double kHybTemporalMiB = 170.0;
 
 struct HybArgs {
   const int64_t *offs;  // [B+1]
@@ -99,6 +107,7 @@ struct HybArgs {
   uint32_t *err;
   uint32_t spin_limit;
   HybLayout lay;      // which data workgroup holds which segment
+  int tslots;         // streamed vectors per row and thread read with the temporal policy (the rest streaming)
 };
 
 // buf_load16 with the default (temporal) cache policy: the line may stay in
@@ -195,16 +204,30 @@ struct Hybrid {
           for (int i = 0; i < K; ++i) sm.lds[X][j][i][t] = stage[j][i];
         }
       }
-      // streamed vectors, NS per row at a time; loaded with the
-      // temporal policy so that the combine's re-read, one bucket later, is
-      // mostly served by the last-level cache instead of HBM
+      // streamed vectors, NS per row at a time.  The first tslots are
+      // loaded with the temporal policy so that the combine's re-read, one
+      // bucket later, is mostly served by the last-level cache instead of
+      // HBM; the rest with the streaming policy, so that a bucket whose
+      // streamed part exceeds that cache does not push them out.
       const int nslot = (sp.nv + T - 1) / T;
-      for (int j0 = NB; j0 < nslot; j0 += NS) {
+      const int jt = NB + a.tslots < nslot ? NB + a.tslots : nslot;
+      int j0 = NB;
+      for (; j0 < jt; j0 += NS) {
         u32x4 q[NS][K];
 #pragma unroll
         for (int u = 0; u < NS; ++u) {
 #pragma unroll
           for (int i = 0; i < K; ++i) q[u][i] = buf_load16_keep(rs[i], voff, (uint32_t)((j0 + u) * T * 16));
+        }
+#pragma unroll
+        for (int u = 0; u < NS; ++u) accumulate_vec(acc, q[u]);
+      }
+      for (; j0 < nslot; j0 += NS) {
+        u32x4 q[NS][K];
+#pragma unroll
+        for (int u = 0; u < NS; ++u) {
+#pragma unroll
+          for (int i = 0; i < K; ++i) q[u][i] = buf_load16(rs[i], voff, (uint32_t)((j0 + u) * T * 16));
         }
 #pragma unroll
         for (int u = 0; u < NS; ++u) accumulate_vec(acc, q[u]);
@@ -523,8 +546,10 @@ hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, con
                          float *weights, double *aux, void *out, double *partials, uint32_t *arrive,
                          uint32_t *flags, uint32_t *err, uint32_t spin_limit, int grid,
                          const HybLayout &layout, hipStream_t s) {
+  const double per_slot = (double)(layout.nslots > 0 ? layout.nslots : 1) * kHybThreads * 16.0 * K;
   const HybArgs a{offs, B, shift, method, iters, c, order, gram, weights, aux, out,
-                  partials, arrive, flags, err, spin_limit, layout};
+                  partials, arrive, flags, err, spin_limit, layout,
+                  (int)(kHybTemporalMiB * (1 << 20) / per_slot)};
 #define BKMOO_HYB_CASE(k)                                                                        \
   case k:                                                                                        \
     if (dt == F32)                                                                               \
