@@ -1,10 +1,11 @@
 """Seeded random small configurations through the same parity checks as the
-hand-picked tests: K = 2..8, fp32 and bf16 inputs, either output type,
+hand-picked tests: K = 2..10, fp32 and bf16 inputs, either output type,
 every method (exact solvers included), 0..20 iterations, CAGrad radii
 0..0.9, 1..47 ragged buckets with empty and one-element ones, aligned and
 unaligned rows, on the automatic path and on each forced path.  The
-cooperative half draws only cases the hybrid kernel can run (K <= 8,
-aligned rows, non-exact methods) and asserts that it ran."""
+cooperative half draws a cooperative kernel first and then only cases it
+can run (K <= 8 for the two-buffer kernel, K <= 10 for the single-buffer
+one, aligned rows, non-exact methods) and asserts that it ran."""
 
 import numpy as np
 import pytest
@@ -20,7 +21,11 @@ BASES = {"bf16": WORKLOADS["llama3-8b-k4-mgda-bf16"], "f32": WORKLOADS["gpt2-124
 
 def _draw(case, cooperative):
     rng = np.random.default_rng(20_261_202 + 1_000 * cooperative + case)
-    K = int(rng.choice([2, 3, 4, 4, 6, 8] if cooperative else [2, 3, 4, 5, 8]))
+    path = str(rng.choice(["PATH_HYBRID", "PATH_REFILL"] if cooperative
+                          else ["auto", "PATH_TWO_PASS", "PATH_HYBRID", "PATH_REFILL"]))
+    Ks = [2, 3, 4, 4, 6, 8] if path == "PATH_HYBRID" else [2, 3, 4, 6, 8, 9, 10] if cooperative \
+        else [2, 3, 4, 5, 8, 10]
+    K = int(rng.choice(Ks))
     dt = str(rng.choice(["bf16", "f32"]))
     methods = ["mgda", "pcgrad", "cagrad", "mean"] + ([] if cooperative else ["mgda-exact", "cagrad-exact"])
     method = str(rng.choice(methods))
@@ -36,15 +41,13 @@ def _draw(case, cooperative):
     if sum(lens) == 0:
         lens[-1] = 16
     out_dt = None if rng.random() < 0.7 else (torch.float32 if dt == "bf16" else torch.bfloat16)
-    path = str(rng.choice(["PATH_HYBRID", "PATH_REFILL"] if cooperative
-                          else ["auto", "PATH_TWO_PASS", "PATH_HYBRID", "PATH_REFILL"]))
     wl = small_workload(BASES[dt], sum(lens), bucket_lens=lens, K=K, dtype=dt, method=method, max_iter=iters,
                         cagrad_c=c, seed=7_000 + 100 * cooperative + case)
     return wl, out_dt, path
 
 
 @pytest.mark.parametrize("cooperative", [False, True])
-@pytest.mark.parametrize("case", range(12))
+@pytest.mark.parametrize("case", range(16))
 def test_random_config(gpu_lib, case, cooperative):
     wl, out_dt, path = _draw(case, cooperative)
     grads, _, _ = to_device_inputs(wl)
