@@ -70,11 +70,14 @@ constexpr uint32_t kWeightPending = 0x7f800001u;
 // streamed per row and step (NS), and kept slots between a refill load and
 // the addition of its products (lag): the registers and LDS the two-buffer
 // kernel spreads over two buckets, as far as they compile without spills.
-// At K = 4 one more kept register vector with a lag of one slot beat seven
+// At K = 4 eight kept register vectors with a lag of one slot beat seven
 // with a lag of two (K=4 bf16 25 MiB MGDA FW-20, two groups: 16.82-16.92
-// against 17.13-17.18 ms).
+// against 17.13-17.18 ms), and nine (4 VGPRs spilled: three scratch
+// stores and three loads in the kernel) beat eight (alternating processes:
+// 16.27-16.50 against 16.56-16.89 ms); ten spill 20 VGPRs and lose
+// (17.05-17.55 ms).
 constexpr int ref_regs(int K) {
-  return K <= 2 ? 16 : K == 3 ? 10 : K == 4 ? 8 : K == 5 ? 4 : K == 6 ? 3 : K <= 8 ? 2 : 1;
+  return K <= 2 ? 16 : K == 3 ? 10 : K == 4 ? 9 : K == 5 ? 4 : K == 6 ? 3 : K <= 8 ? 2 : 1;
 }
 constexpr int ref_lds(int K) { return K <= 2 ? 8 : K <= 4 ? 4 : K <= 8 ? 2 : 1; }
 constexpr int ref_stream(int K) { return K <= 7 ? 2 : 1; }
