@@ -605,7 +605,7 @@ bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_
     if (g <= 0) return BKMOO_EUNSUPPORTED;
     const int groups = refill_groups(K, (int)dt, N, B);
     const HybLayout lay{(g - refill_solvers(groups)) / groups, 0, 0, 0};
-    const int64_t unit = hybrid_unit_elems((int)dt), held_max = refill_held_elems(K, (int)dt);
+    const int64_t unit = hybrid_unit_elems((int)dt), held_max = refill_held_elems(K, (int)dt, (int)out_dt);
     const int64_t smin = (int64_t)refill_stream_min() * unit;
     uint64_t reread = 0;
     for (int b = 0; b < B; ++b) {  // each segment re-reads what it did not keep

@@ -14,7 +14,7 @@ constexpr int kRefMaxGroups = 32;  // bucket groups (and solvers) at most
 // Its data workgroups hold equal segments; refill_stream_min() vectors per
 // row and thread of each segment are always streamed.
 int refill_grid(int K, int dt, int out_dt);
-int64_t refill_held_elems(int K, int dt);
+int64_t refill_held_elems(int K, int dt, int out_dt);
 int refill_stream_min();
 // Streamed vectors per row and thread a data workgroup reads with the
 // temporal cache policy, for `groups` groups over a grid of `grid`.

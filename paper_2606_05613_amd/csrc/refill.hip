@@ -75,9 +75,15 @@ constexpr uint32_t kWeightPending = 0x7f800001u;
 // against 17.13-17.18 ms), and nine (4 VGPRs spilled: three scratch
 // stores and three loads in the kernel) beat eight (alternating processes:
 // 16.27-16.50 against 16.56-16.89 ms); ten spill 20 VGPRs and lose
-// (17.05-17.55 ms).
-constexpr int ref_regs(int K) {
-  return K <= 2 ? 16 : K == 3 ? 10 : K == 4 ? 9 : K == 5 ? 4 : K == 6 ? 3 : K <= 8 ? 2 : 1;
+// (17.05-17.55 ms).  At K = 9 and 10 with fp32 in and out a second kept
+// register vector (13 VGPRs spilled at K = 10) beat one (K=10 fp32, MGDA
+// FW-20, alternating processes: 1 MiB buckets 16.5-16.6 against 18.2-18.3
+// ms, 5 MiB 17.5 against 18.8, 25 MiB 19.2 against 20.3-20.5, 100 MiB 21.5
+// against 24.7); with bf16 on either side it spills 80-140 VGPRs (bf16 in
+// and out spills 50 already with one).
+constexpr int ref_regs(int K, int DT, int ODT) {
+  return K <= 2 ? 16 : K == 3 ? 10 : K == 4 ? 9 : K == 5 ? 4 : K == 6 ? 3 : K <= 8 ? 2
+       : DT == F32 && ODT == F32 ? 2 : 1;
 }
 constexpr int ref_lds(int K) { return K <= 2 ? 8 : K <= 4 ? 4 : K <= 8 ? 2 : 1; }
 constexpr int ref_stream(int K) { return K <= 7 ? 2 : 1; }
@@ -155,7 +161,7 @@ __device__ bool poll_record(const uint32_t *rec, uint32_t (&x)[K], const RefArgs
 template <int K, int DT, int ODT>
 struct Refill {
   static constexpr int V = vec_elems(DT);
-  static constexpr int NR = ref_regs(K);
+  static constexpr int NR = ref_regs(K, DT, ODT);
   static constexpr int NL = ref_lds(K);
   static constexpr int NB = NR + NL;
   static constexpr int NS = ref_stream(K);
@@ -671,8 +677,8 @@ int refill_temporal_slots(int K, int dt, int grid, int groups) {
 // another's unfinished one).
 int refill_solvers(int groups) { return groups < kHybridSolvers ? kHybridSolvers : groups; }
 
-int64_t refill_held_elems(int K, int dt) {
-  return (int64_t)kRefThreads * (ref_regs(K) + ref_lds(K)) * vec_elems(dt);
+int64_t refill_held_elems(int K, int dt, int out_dt) {
+  return (int64_t)kRefThreads * (ref_regs(K, dt, out_dt) + ref_lds(K)) * vec_elems(dt);
 }
 
 hipError_t launch_refill(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
