@@ -251,8 +251,8 @@ bkmoo_status bkmoo_combine(int32_t K, const void *const *grads, bkmoo_dtype dt, 
  * plus 4 MiB per us of L; refill (K <= 10) for at least 8 buckets whose
  * round of G buckets holds at least 64 + 2 L MiB and, for G > 1, at most
  * 300 MiB (a round the Infinity Cache still serves).  Hybrid where it
- * is eligible, except refill for K <= 4 with L >= 4 us; else refill where
- * eligible; else the two passes.  Exact solvers never take a cooperative
+ * is eligible, except refill for K = 3 and for K <= 4 with L >= 4 us; else
+ * refill where eligible; else the two passes.  Exact solvers never take a cooperative
  * path.
  * bkmoo_resolve_path reports the choice; bkmoo_set_resolve_path forces one.
  */

@@ -303,7 +303,13 @@ constexpr double kRefillMinRoundMiB = 64.0, kRefillMiBPerUs = 2.0;
 // 5.24 / 5.02; K=4 12.5 MiB (328) MGDA 5.66 / 4.52 (G=4); K=3 25 MiB (328)
 // MGDA 5.24 / 4.79 (G=2), CAGrad 5.48 / 5.04; K=2 25 MiB (328) MGDA FW-20
 // (2.8 us) 5.52 / 5.83 (G=4), CAGrad 6.83 / 5.70; K=6 MGDA 3.42 / 3.75; K=8
-// CAGrad FW-20 36.4 / 39.4 (G=1), 41.0 (G=2).
+// CAGrad FW-20 36.4 / 39.4 (G=1), 41.0 (G=2).  With nine kept register
+// vectors at K=4 (one process each, ms): K=4 25 MiB mean 16.03 / 17.09,
+// PCGrad 16.15 / 16.91, MGDA FW-20 17.39 / 16.58, CAGrad 18.97 / 16.94;
+// K=4 fp32 GPT-2 shape (19 buckets) PCGrad 0.54 / 0.56, CAGrad 0.63 /
+// 0.59; K=2 25 MiB mean 5.59 / 5.86, MGDA 5.47 / 5.83, CAGrad 6.79 / 5.70;
+// K=3 25 MiB mean 5.21 / 5.01, PCGrad 5.26 / 4.93, MGDA 5.23 / 4.78,
+// CAGrad 5.49 / 5.04: at K = 3 the refill kernel wins for every method.
 constexpr double kRefillOverHybridUs = 4.0;
 
 int refill_groups(int K, int dt, int64_t N, int B) {
@@ -339,7 +345,7 @@ int pick_path(int K, int dt, int out_dt, int64_t N, int B, bool vec, int method,
               int *grid) {
   const int rg = choose_refill(K, dt, out_dt, N, B, vec, method, iters);
   const int hg = choose_hybrid(K, dt, out_dt, N, B, vec, method, iters, cap_slots);
-  const bool prefer_refill = K <= 4 && solve_latency_us(method, K, iters) >= kRefillOverHybridUs;
+  const bool prefer_refill = K == 3 || (K <= 4 && solve_latency_us(method, K, iters) >= kRefillOverHybridUs);
   if (rg > 0 && (hg <= 0 || prefer_refill || g_resolve_path.load() == BKMOO_PATH_REFILL)) {
     *grid = rg;
     return BKMOO_PATH_REFILL;

@@ -7,7 +7,8 @@ PCGrad).  The refill path (K <= 10) needs at least 8 buckets and a round of
 its G = clamp(round(180 MiB / bucket), 1, 32) groups' buckets of at least
 64 + 2 L MiB and, with more than one group, at most 300 MiB; it runs where
 the hybrid path does not, and instead
-of it for K <= 4 with L >= 4 us.  Everything else runs the two passes.
+of it for K = 3 and for K <= 4 with L >= 4 us.  Everything else runs the
+two passes.
 Only shapes are used (no resolve runs); the cases sit away from the
 thresholds."""
 
@@ -114,6 +115,17 @@ def test_hybrid_needs_a_tenth_on_chip(gpu_lib):
     gpu_lib.set_resolve_path(0)
     assert gpu_lib.resolve_path(g, 9, "mean", 0) == gpu_lib.PATH_REFILL
     assert gpu_lib.resolve_path(g, 33, "mean", 0) == gpu_lib.PATH_HYBRID
+
+
+def test_three_tasks_take_the_refill_kernel(gpu_lib):
+    """K=3 bf16 rows of 2^28 elements in 8 buckets (192 MiB each, one
+    group) and 32 (48 MiB, four groups): the single-buffer kernel for every
+    method, also where the two-buffer kernel could run."""
+    g = torch.empty((3, 1 << 28), dtype=torch.bfloat16, device="cuda")
+    gpu_lib.set_resolve_path(0)
+    for B in (8, 32):
+        for method, iters in (("mean", 0), ("pcgrad", 0), ("mgda", 20), ("cagrad", 20)):
+            assert gpu_lib.resolve_path(g, B + 1, method, iters) == gpu_lib.PATH_REFILL, (B, method)
 
 
 def test_misaligned_rows_take_the_two_passes(gpu_lib):
