@@ -213,7 +213,7 @@ constexpr double kHybridSkewMaxRowBytes = 32.0 * (1 << 20);
 constexpr double kHybridSkewMinUs = 4.0, kHybridSkewMaxUs = 9.0;
 constexpr double kHybridLightMinUs = 3.0;
 
-int hybrid_skew_pm(int K, int dt, int method, int iters, int64_t N, int B, int grid) {
+int hybrid_skew_pm(int K, int dt, int out_dt, int method, int iters, int64_t N, int B, int grid) {
   if (K != 4 || (method != BKMOO_MGDA && method != BKMOO_CAGRAD) || iters <= 0 || B <= 0) return 0;
   const double lat = solve_latency_us(method, K, iters);
   if (lat < kHybridSkewMinUs || lat >= kHybridSkewMaxUs) return 0;
@@ -222,7 +222,7 @@ int hybrid_skew_pm(int K, int dt, int method, int iters, int64_t N, int B, int g
   const int gd = hybrid_data_workgroups(grid), older = hybrid_older_workgroups(grid);
   if (older <= 0 || older >= gd) return 0;
   // the second workgroups' segments must still fill their on-chip share
-  const int64_t unit = hybrid_unit_elems(dt), nb = hybrid_held_elems(K, dt) / unit;
+  const int64_t unit = hybrid_unit_elems(dt), nb = hybrid_held_elems(K, dt, out_dt) / unit;
   const int64_t nu = (int64_t)(avg / unit);
   const int64_t co = (nu * (1000 + kHybridSkewPm) + (int64_t)gd * 1000 - 1) / ((int64_t)gd * 1000);
   const int64_t rest = nu - (int64_t)older * co;
@@ -231,10 +231,10 @@ int hybrid_skew_pm(int K, int dt, int method, int iters, int64_t N, int B, int g
 }
 
 // The hybrid kernel's layout for one call (grid from hybrid_grid).
-HybLayout hybrid_layout(int K, int dt, int method, int iters, int64_t N, int B, int grid) {
+HybLayout hybrid_layout(int K, int dt, int out_dt, int method, int iters, int64_t N, int B, int grid) {
   HybLayout L{hybrid_data_workgroups(grid), hybrid_older_workgroups(grid), 0, 0};
   if (L.older <= 0 || L.older + kHybridSolvers >= L.nslots) return L;
-  L.skew_pm = hybrid_skew_pm(K, dt, method, iters, N, B, grid);
+  L.skew_pm = hybrid_skew_pm(K, dt, out_dt, method, iters, N, B, grid);
   if (L.skew_pm == 0 && (method == BKMOO_MGDA || method == BKMOO_CAGRAD) &&
       solve_latency_us(method, K, iters) >= kHybridLightMinUs) {
     L.light = 1;
@@ -260,7 +260,7 @@ int choose_hybrid(int K, int dt, int out_dt, int64_t N, int B, bool vec, int met
   if (mode == BKMOO_PATH_HYBRID) return g;
   const double avg_elems = (double)N / B;
   const double bucket_bytes = avg_elems * K * elem_bytes(dt);
-  const double held = (double)hybrid_held_elems(K, dt) * gd / (avg_elems > 1.0 ? avg_elems : 1.0);
+  const double held = (double)hybrid_held_elems(K, dt, out_dt) * gd / (avg_elems > 1.0 ? avg_elems : 1.0);
   const double base_mib = kHybridBaseMiB > kHybridBaseMiBPerRow * K ? kHybridBaseMiB : kHybridBaseMiBPerRow * K;
   const double min_bytes = (base_mib + kHybridMiBPerUs * solve_latency_us(method, K, iters)) * (1 << 20);
   return B >= kHybridMinBuckets && bucket_bytes >= min_bytes && held >= kHybridMinHeld ? g : 0;
@@ -533,7 +533,7 @@ bkmoo_status resolve_impl(int32_t K, const void *const *grads, bkmoo_dtype dt, i
     if (e != hipSuccess) return BKMOO_EHIP;
     e = launch_hybrid(K, (int)dt, (int)out_dt, grads, bucket_offsets, B, shift, (int)method, iters, c,
                       order, G, W, aux, out, w.partials, w.sync, w.sync + B * kSyncStride, w.err, g_spin_limit.load(),
-                      hgrid, hybrid_layout(K, (int)dt, (int)method, iters, N, B, hgrid), stream);
+                      hgrid, hybrid_layout(K, (int)dt, (int)out_dt, (int)method, iters, N, B, hgrid), stream);
     return hip_status(e);
   }
 
@@ -637,8 +637,8 @@ bkmoo_status bkmoo_resolve_traffic(int32_t K, int64_t N, int32_t B, const int64_
   {
     const int g = hybrid_grid(K, (int)dt, (int)out_dt);
     if (g <= 0) return BKMOO_EUNSUPPORTED;
-    const HybLayout lay = hybrid_layout(K, (int)dt, (int)method, max_iter, N, B, g);
-    const int64_t unit = hybrid_unit_elems((int)dt), held = hybrid_held_elems(K, (int)dt);
+    const HybLayout lay = hybrid_layout(K, (int)dt, (int)out_dt, (int)method, max_iter, N, B, g);
+    const int64_t unit = hybrid_unit_elems((int)dt), held = hybrid_held_elems(K, (int)dt, (int)out_dt);
     for (int b = 0; b < B; ++b) {  // each segment re-reads what it did not keep
       const int64_t n = offsets_host[b + 1] - offsets_host[b];
       int64_t lo, hi, nseg, ns;

@@ -79,7 +79,13 @@ constexpr int kHybRedBatch = 24;
 // with fewer than ~10 in flight the kernel falls behind the two passes
 // (K = 5 and 6 with NS = 1: 5-25% slower; with NS = 2 and NR = 2: 8-30%
 // faster).  K = 8 fits only NR = NL = NS = 1 (its 8 loads in flight).
-constexpr int hyb_regs(int K) { return K <= 2 ? 9 : K == 3 ? 6 : K == 4 ? 4 : K <= 6 ? 2 : 1; }
+// With the lane-parallel solvers one more register vector fits without
+// spills at K = 5 (bf16, 25 MiB per row, MGDA FW-20: 4.44-4.49 against 5.40
+// ms) and at K = 4 with fp32 in and out (GPT-2 shape, PCGrad: 0.515-0.524
+// against 0.528-0.541 ms; 1% slower with 41 buckets of 100 MiB).
+constexpr int hyb_regs(int K, int DT, int ODT) {
+  return K <= 2 ? 9 : K == 3 ? 6 : K == 4 ? (DT == F32 && ODT == F32 ? 5 : 4) : K == 5 ? 3 : K == 6 ? 2 : 1;
+}
 constexpr int hyb_lds(int K) { return K <= 2 ? 4 : K <= 4 ? 2 : 1; }
 constexpr int hyb_stream(int K) { return K <= 7 ? 2 : 1; }
 // Streamed bytes per bucket (all data workgroups) read with the temporal
@@ -139,7 +145,7 @@ __device__ bool wait_at_least(const uint32_t *p, uint32_t target, const HybArgs 
 template <int K, int DT, int ODT>
 struct Hybrid {
   static constexpr int V = vec_elems(DT);
-  static constexpr int NR = hyb_regs(K);
+  static constexpr int NR = hyb_regs(K, DT, ODT);
   static constexpr int NL = hyb_lds(K);
   static constexpr int NB = NR + NL;
   static constexpr int NS = hyb_stream(K);
@@ -535,8 +541,8 @@ int hybrid_older_workgroups(int grid) {
   return grid == 2 * cus && cus > kHybridSolvers ? cus - kHybridSolvers : 0;
 }
 
-int64_t hybrid_held_elems(int K, int dt) {
-  return (int64_t)kHybThreads * (hyb_regs(K) + hyb_lds(K)) * vec_elems(dt);
+int64_t hybrid_held_elems(int K, int dt, int out_dt) {
+  return (int64_t)kHybThreads * (hyb_regs(K, dt, out_dt) + hyb_lds(K)) * vec_elems(dt);
 }
 
 int64_t hybrid_unit_elems(int dt) { return (int64_t)kHybThreads * vec_elems(dt); }

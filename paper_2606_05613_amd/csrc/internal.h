@@ -216,7 +216,7 @@ struct HybLayout {
 };
 // Elements of its segment a data workgroup keeps on chip per bucket, and the
 // granule segment lengths are rounded up to.
-int64_t hybrid_held_elems(int K, int dt);
+int64_t hybrid_held_elems(int K, int dt, int out_dt);
 int64_t hybrid_unit_elems(int dt);
 hipError_t launch_hybrid(int K, int dt, int out_dt, const void *const *rows, const int64_t *offs, int B,
                          int shift, int method, int iters, double c, const int8_t *order, double *gram,

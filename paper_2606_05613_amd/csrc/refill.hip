@@ -81,8 +81,11 @@ constexpr uint32_t kWeightPending = 0x7f800001u;
 // ms, 5 MiB 17.5 against 18.8, 25 MiB 19.2 against 20.3-20.5, 100 MiB 21.5
 // against 24.7); with bf16 on either side it spills 80-140 VGPRs (bf16 in
 // and out spills 50 already with one).
+// At K = 5..7 more register vectors fit without spills (bf16, 5 MiB per
+// row, MGDA FW-20: K=5 six 4.60 against four 4.89 ms, K=7 three 4.75
+// against two 4.95; K=6 five spill 2-12 VGPRs and gain nothing).
 constexpr int ref_regs(int K, int DT, int ODT) {
-  return K <= 2 ? 16 : K == 3 ? 10 : K == 4 ? 9 : K == 5 ? 4 : K == 6 ? 3 : K <= 8 ? 2
+  return K <= 2 ? 16 : K == 3 ? 10 : K == 4 ? 9 : K == 5 ? 6 : K == 6 ? 4 : K == 7 ? 3 : K == 8 ? 2
        : DT == F32 && ODT == F32 ? 2 : 1;
 }
 constexpr int ref_lds(int K) { return K <= 2 ? 8 : K <= 4 ? 4 : K <= 8 ? 2 : 1; }
