@@ -561,37 +561,44 @@ __device__ double lane_solve_mgda(const double *G, int iters, int lane) {
 }
 
 // CAGrad (as solve_cagrad and cagrad_primal).  Lane i < K returns task i's
-// combine weight in *wt and dual variable in *w_out.
+// combine weight in *wt and dual variable in *w_out.  The step's
+// quantities are carried from one iteration to the next instead of being
+// summed again: with w' = (1 - gamma) w + gamma e_s, (G w')_i = (1 - gamma)
+// (G w)_i + gamma G_is, w'^T G w' is the line search's quadratic at gamma
+// and b^T w' = (1 - gamma) b^T w + gamma b_s (exact for gamma = 0 and, but
+// for the quadratic, gamma = 1); the first iterate's sums are computed as
+// before.
 template <int K>
 __device__ void lane_solve_cagrad(const double *G, int iters, double c, int lane, double *wt, double *w_out) {
   const bool task = lane < K;
   const int me = task ? lane : 0;
   const double invK = 1.0 / (double)K;
-  double gi[K], w[K];
+  double gi[K];
   double gd = 0.0, rs = 0.0;
 #pragma unroll
   for (int j = 0; j < K; ++j) {
     gi[j] = task ? G[me * K + j] : 0.0;
     gd = j == me ? gi[j] : gd;
     rs += gi[j];
-    w[j] = invK;
   }
   const double bo = rs / (double)K;  // b_i = (G 1)_i / K
   double g0sq = row_sum<K>(task ? rs : 0.0) / (double)(K * K);
   g0sq = g0sq > 0.0 ? g0sq : 0.0;
   const double r = c * sqrt(g0sq);
   double own = task ? invK : 0.0;
-  for (int it = 0; it < iters; ++it) {
-    double v = 0.0;
+  double v = 0.0;  // (G w)_i
 #pragma unroll
-    for (int j = 0; j < K; ++j) v += gi[j] * w[j];
-    const double cq = row_sum<K>(task ? own * v : 0.0);
-    const double bw = row_sum<K>(task ? bo * own : 0.0);
+  for (int j = 0; j < K; ++j) v += gi[j] * invK;
+  double cq = row_sum<K>(task ? own * v : 0.0);   // w^T G w
+  double bw = row_sum<K>(task ? bo * own : 0.0);  // b^T w
+  for (int it = 0; it < iters; ++it) {
     const double nrm = sqrt(cq > 0.0 ? cq : 0.0);
     const double grad = bo + (nrm > 1e-300 ? r * v / nrm : 0.0);
     const int s = row_argmin<K>(task ? grad : __builtin_inf(), task ? lane : kWave);
+    const double gis = task ? G[me * K + s] : 0.0;
     const double vs = lane_f64(v, s);
-    const double beta1 = lane_f64(bo, s) - bw;
+    const double bs = lane_f64(bo, s);
+    const double beta1 = bs - bw;
     const double A = lane_f64(gd, s) - 2.0 * vs + cq;
     const double Bq = vs - cq;
     double g1 = -1.0, g2 = -1.0;
@@ -609,27 +616,22 @@ __device__ void lane_solve_cagrad(const double *G, int iters, double c, int lane
     const int q4 = lane & 3;
     const double gc = q4 == 0 ? 0.0 : q4 == 1 ? g1 : q4 == 2 ? g2 : 1.0;
     const bool valid = lane < 4 && (q4 == 0 || q4 == 3 || (gc > 0.0 && gc < 1.0));
-    double qq = A * gc * gc + 2.0 * Bq * gc + cq;
-    qq = qq > 0.0 ? qq : 0.0;
+    const double qraw = A * gc * gc + 2.0 * Bq * gc + cq;
+    const double qq = qraw > 0.0 ? qraw : 0.0;
     const double f = valid ? bw + beta1 * gc + r * sqrt(qq) : __builtin_inf();
     double fv = f;
     int fi = valid ? q4 : kWave;
     argmin_step<kDppXor1>(fv, fi);
     argmin_step<kDppXor2>(fv, fi);
-    const double gamma = lane_f64(gc, __builtin_amdgcn_readlane(fi, 0));
-#pragma unroll
-    for (int j = 0; j < K; ++j) {
-      double nw = (1.0 - gamma) * w[j];
-      if (j == s) nw += gamma;
-      w[j] = nw;
-    }
+    const int win = __builtin_amdgcn_readlane(fi, 0);
+    const double gamma = lane_f64(gc, win);
+    cq = lane_f64(qraw, win);
+    v = (1.0 - gamma) * v + gamma * gis;
+    bw = (1.0 - gamma) * bw + gamma * bs;
     double no = (1.0 - gamma) * own;
     if (task && lane == s) no += gamma;
     own = no;
   }
-  double v = 0.0;
-#pragma unroll
-  for (int j = 0; j < K; ++j) v += gi[j] * w[j];
   const double q = row_sum<K>(task ? own * v : 0.0);
   double dmax = 0.0;
 #pragma unroll
