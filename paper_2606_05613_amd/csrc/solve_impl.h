@@ -522,12 +522,15 @@ __device__ __forceinline__ void lane_best_pair(const double *G, int lane, int &b
 }
 
 // MGDA (as solve_mgda).  G: K x K row-major, readable by every lane (LDS).
-// Lane i < K returns task i's simplex weight.
+// Lane i < K returns task i's simplex weight.  G a and a^T G a are summed
+// for the starting pair's point and then carried: with a' = g a + (1 - g)
+// e_t, (G a')_i = g (G a)_i + (1 - g) G_it and a'^T G a' = g^2 a^T G a +
+// 2 g (1 - g) (G a)_t + (1 - g)^2 G_tt (exact for g = 1 and g = 0).
 template <int K>
 __device__ double lane_solve_mgda(const double *G, int iters, int lane) {
   const bool task = lane < K;
   const int me = task ? lane : 0;
-  double gi[K], a[K];
+  double gi[K];
   double gd = 0.0;
 #pragma unroll
   for (int j = 0; j < K; ++j) {
@@ -537,24 +540,21 @@ __device__ double lane_solve_mgda(const double *G, int iters, int lane) {
   int bi, bj;
   double bg;
   lane_best_pair<K>(G, lane, bi, bj, bg);
-#pragma unroll
-  for (int j = 0; j < K; ++j) a[j] = j == bi ? bg : j == bj ? 1.0 - bg : 0.0;
   double own = task ? (me == bi ? bg : me == bj ? 1.0 - bg : 0.0) : 0.0;
+  double v = 0.0;  // (G a)_i
+#pragma unroll
+  for (int j = 0; j < K; ++j) v += gi[j] * (j == bi ? bg : j == bj ? 1.0 - bg : 0.0);
+  double aa = row_sum<K>(task ? own * v : 0.0);  // a^T G a
   for (int it = 0; it < iters; ++it) {
-    double v = 0.0;
-#pragma unroll
-    for (int j = 0; j < K; ++j) v += gi[j] * a[j];
     const int t = row_argmin<K>(task ? v : __builtin_inf(), task ? lane : kWave);
-    const double aa = row_sum<K>(task ? own * v : 0.0);
-    const double g = pair_gamma(aa, lane_f64(v, t), lane_f64(gd, t));
-#pragma unroll
-    for (int j = 0; j < K; ++j) {
-      double na = g * a[j];
-      if (j == t) na += 1.0 - g;
-      a[j] = na;
-    }
+    const double git = task ? G[me * K + t] : 0.0;
+    const double vt = lane_f64(v, t), gtt = lane_f64(gd, t);
+    const double g = pair_gamma(aa, vt, gtt);
+    const double h = 1.0 - g;
+    aa = g * g * aa + 2.0 * g * h * vt + h * h * gtt;
+    v = g * v + h * git;
     double no = g * own;
-    if (task && lane == t) no += 1.0 - g;
+    if (task && lane == t) no += h;
     own = no;
   }
   return own;
