@@ -1,9 +1,10 @@
-"""The pipelined, partly resident (hybrid) resolve kernel against the
-oracle.  Every method and input type for K = 2..8, ragged and unaligned
-buckets, 1 to 41 buckets (the kernel alternates two buffers), full 25 MiB
-buckets (whose segments stream part of their data), a bucket larger than
-the chip holds, determinism, agreement with the two-pass path, and the
-bounded waits' timeout forced from the host."""
+"""The pipelined, partly resident resolve kernels (two-buffer and
+single-buffer) against the oracle.  Every method and input type for K =
+2..10, ragged and unaligned buckets, 1 to 41 buckets (the two-buffer kernel
+alternates two buffers), full 25 MiB buckets and buckets long enough that
+every kept vector holds data (their segments stream the rest), a bucket
+larger than the chip holds, determinism, agreement with the two-pass path,
+and the bounded waits' timeout forced from the host."""
 
 import numpy as np
 import pytest
@@ -164,6 +165,41 @@ def test_hybrid_solver_mates_hold_no_segment(gpu_lib, dtype):
     mates, even = traffic("cagrad", 20), traffic("mean", 0)
     assert mates != even
     assert traffic("mgda", 5) == even and traffic("pcgrad", 0) == even
+
+
+# Vectors per task row and thread a segment needs so that every kept
+# register and LDS vector of either kernel holds data and the rest streams
+# (the single-buffer kernel always streams four; its largest kept counts
+# are 24 at K = 2, 14 at K = 3, 13 at K = 4, 8 at K = 5, fewer above).
+_SLOTS = {2: 30, 3: 19, 4: 18, 5: 13, 6: 11, 7: 10, 8: 9, 9: 8, 10: 8}
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("K,path_name", [(K, "PATH_HYBRID") for K in range(2, 9)]
+                         + [(K, "PATH_REFILL") for K in range(2, 11)])
+def test_coop_every_kept_slot(gpu_lib, K, path_name, dtype):
+    """Two ragged buckets of _SLOTS[K] vectors per row, thread and data
+    workgroup: every kept register and LDS vector holds data and part of
+    each segment streams (the bytes requested exceed the one-read floor),
+    for K = 2..10, both input types and one method per K, against the
+    oracle."""
+    path = getattr(gpu_lib, path_name)
+    V = 8 if dtype == "bf16" else 4
+    n = 508 * 256 * V * _SLOTS[K]
+    method = ("mgda", "cagrad", "pcgrad", "mean")[K % 4]
+    wl = small_workload(BASE, 2 * n + 8, bucket_lens=[n + 3, n + 5], K=K, dtype=dtype, method=method,
+                        seed=9300 + 10 * K + (dtype == "bf16"))
+    s = 2 if dtype == "bf16" else 4
+    gpu_lib.set_resolve_path(path)
+    try:
+        grads, _, _ = to_device_inputs(wl)
+        assert gpu_lib.resolve_path(grads, wl.B + 1, method, wl.max_iter) == path
+        floor = (K + 1) * s * wl.N
+        assert gpu_lib.resolve_traffic(K, wl.offsets(), dtype, path, method=method, max_iter=wl.max_iter) > floor
+        print(f"case {path_name} K={K} {dtype} {method} N={wl.N}", full_parity(gpu_lib, wl, grads=grads),
+              flush=True)
+    finally:
+        gpu_lib.set_resolve_path(0)
 
 
 def test_coop_bucket_larger_than_chip(coop):
