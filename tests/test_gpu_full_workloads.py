@@ -25,6 +25,7 @@ At these sizes the oracle cannot redo everything, so each workload checks:
   the gradients were drawn with (sampling error ~1/sqrt(n_b) ~ 3e-4).
 """
 
+import dataclasses
 import gc
 
 import numpy as np
@@ -188,6 +189,36 @@ def test_full_workload(gpu_lib, name):
     assert gpu_lib.resolve_path(grads, wl.B + 1, wl.method, wl.max_iter) == getattr(gpu_lib, EXPECTED_PATH[name])
     try:
         _check_workload(gpu_lib, wl, grads, offs, order)
+    finally:
+        del grads
+        _free()
+
+
+# the other methods on the two Llama-3-8B-shaped draws, and the path each
+# takes at that shape
+OTHER_METHODS = {
+    "llama3-8b-k4-mgda-bf16": {"pcgrad": "PATH_HYBRID", "cagrad": "PATH_REFILL", "mean": "PATH_HYBRID"},
+    "llama3-8b-k8-cagrad-bf16": {"mgda": "PATH_HYBRID", "pcgrad": "PATH_HYBRID"},
+}
+
+
+@pytest.mark.parametrize("name", list(OTHER_METHODS))
+def test_full_llama_shapes_other_methods(gpu_lib, name):
+    """The Llama-3-8B-shaped gradients (K=4 and K=8 bf16, 613 buckets of 25
+    MiB) with the methods their workloads do not name, on the path the
+    automatic choice gives each, through the same full-size checks."""
+    _free()
+    base = WORKLOADS[name]
+    grads = fill_grads(base, device="cuda")
+    offs = torch.from_numpy(base.offsets()).cuda()
+    gpu_lib.set_resolve_path(0)
+    try:
+        grams = {}
+        for m, path in OTHER_METHODS[name].items():
+            wl = dataclasses.replace(base, name=f"{name}/{m}", method=m)
+            assert gpu_lib.resolve_path(grads, wl.B + 1, m, wl.max_iter) == getattr(gpu_lib, path), m
+            order = torch.from_numpy(wl.orders()).cuda() if m == "pcgrad" else None
+            _check_workload(gpu_lib, wl, grads, offs, order, grams)
     finally:
         del grads
         _free()
