@@ -1,5 +1,6 @@
-"""bench.py's host-side contract, without a GPU: the multi-GPU refusal and
-the committed counter summaries matching the kernel sources they describe."""
+"""bench.py's host-side contract, without a GPU: the multi-GPU refusal, the
+committed counter summaries matching the kernel sources they describe, and
+every profile summary's command running committed files only."""
 
 import glob
 import os
@@ -31,3 +32,22 @@ def test_committed_counter_summaries_match_the_kernel_sources():
             f"{os.path.basename(path)} was taken on other {kernel} sources: retake it"
         workload = os.path.basename(path)[len(kernel) + 1:-len("_pmc.md")]
         assert bench.committed_traffic(workload, kernel) is not None, path
+
+
+def test_profile_summaries_name_commands_that_run_committed_files():
+    """Every summary under profiles/ gives the rocprofv3 command it came
+    from, and that command runs bench.py from the repository with a workload
+    bench.py defines (nothing outside the committed tree)."""
+    import bench  # noqa: F401  (the workloads bench.py can run)
+    from synth import WORKLOADS
+    found = sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md")))
+    assert found
+    for path in found:
+        cmds = re.findall(r"^rocprofv3 .*$", open(path).read(), re.M)
+        assert cmds, f"{os.path.basename(path)}: no command"
+        for cmd in cmds:
+            prog = cmd.split(" -- ", 1)[1].split()
+            assert prog[:2] == ["python3", "$REPO/bench.py"], f"{os.path.basename(path)}: {cmd}"
+            wl = prog[prog.index("--workload") + 1]
+            assert wl in WORKLOADS, f"{os.path.basename(path)}: unknown workload {wl}"
+            assert "_work" not in cmd, f"{os.path.basename(path)}: {cmd}"
